@@ -15,6 +15,8 @@ Contents, each function citing the passage of the paper it follows:
 * ``erc``      -- the ERC-LG pipeline of Algorithm 1: right-hand sides
   Y = B^T W^{1/2} Q, column-wise CG on L + eps*I (Eq. 5), squared edge distances
   (Eq. 6), node/edge curvature (Eq. 2) and the sampling weights of Eqs. 7-8.
+* ``accurate`` -- inner products in twice the working precision (Dot2 of Ogita,
+  Rump & Oishi 2005), used by the CG recurrences.
 * ``exact``    -- exact references used to pin the above: pseudoinverse resistance
   (Eq. 1), the dense diagonal-perturbation inverse and the dense-solve JL estimate.
 * ``parallel`` -- a column-parallel driver for the large workloads (columns are
@@ -23,7 +25,7 @@ Contents, each function citing the passage of the paper it follows:
 Parity pins are in tests/test_oracle_*.py.  The projection signs have no values in
 the paper; they are pinned by SplitMix64's published output vectors.
 """
-from . import hashing, graph, erc, exact  # noqa: F401
+from . import hashing, graph, accurate, erc, exact  # noqa: F401
 from .erc import (  # noqa: F401
     rhs, laplacian_apply, cg_columns, edge_distances, resistance, curvature,
     sampling_probs, run,

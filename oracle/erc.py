@@ -12,6 +12,7 @@ Steps, in the paper's order:
    (Section 3.2).
 
 Readings where the paper is silent (each also listed in the design notes):
+CG inner products are computed in twice the working precision (``accurate``);
 CG starts from Z = 0 and stops on the recursively updated residual,
 ||r|| <= tau ||y|| per column; the sum in step 1 runs over each node's neighbours in
 ascending order in fp64 and is rounded once to the working precision; a column whose
@@ -27,6 +28,7 @@ import numpy as np
 
 from . import graph as GR
 from . import hashing as H
+from .accurate import dot2_columns
 
 
 def working_dtype(dtype: str):
@@ -88,13 +90,14 @@ def cg_columns(L, delta: float, Y: np.ndarray, tol: float, max_iter: int) -> CGR
     q = (L + delta I) p, alpha = rho / (p.q), z += alpha p, r -= alpha q,
     rho' = r.r; the column stops once rho' <= tol^2 * rho_0, else
     p = r + (rho'/rho) p.  A column with rho_0 = 0 is converged with z = 0.
+    Inner products are evaluated in twice the working precision (``dot2_columns``).
     """
     Y = np.asarray(Y, dtype=np.float64)
     n, k = Y.shape
     Z = np.zeros((n, k))
     R = Y.copy()
     P = R.copy()
-    rho = np.einsum("ij,ij->j", R, R)
+    rho = dot2_columns(R, R)
     rho0 = rho.copy()
     thr = tol * tol * rho0
     active = rho0 > 0
@@ -105,14 +108,14 @@ def cg_columns(L, delta: float, Y: np.ndarray, tol: float, max_iter: int) -> CGR
             break
         Pa = P[:, a]
         Qa = laplacian_apply(L, delta, Pa)
-        pi = np.einsum("ij,ij->j", Pa, Qa)
+        pi = dot2_columns(Pa, Qa)
         if np.any(~np.isfinite(pi)) or np.any(pi <= 0):
             raise CGBreakdown(f"p.q <= 0 or non-finite at iteration {it}")
         alpha = rho[a] / pi
         Z[:, a] += alpha * Pa
         Ra = R[:, a] - alpha * Qa
         R[:, a] = Ra
-        rho_new = np.einsum("ij,ij->j", Ra, Ra)
+        rho_new = dot2_columns(Ra, Ra)
         iters[a] = it
         done = rho_new <= thr[a]
         beta = rho_new / rho[a]
