@@ -107,13 +107,16 @@ def _connected(g: G.CSRGraph) -> bool:
     return connected_components(A, directed=False)[0] == 1
 
 
-def make_graph(name: str, use_cache: bool = True) -> G.CSRGraph:
+def make_graph(name: str, use_cache: bool = True, progress=None) -> G.CSRGraph:
     """Generate (or load the cached copy of) the graph of workload ``name``."""
     wl = CONFIGS[name]
-    path = os.path.join(cache_dir(), f"{name}_v1.npz")
+    path = os.path.join(cache_dir(), f"{name}_v2.npz")
     if use_cache and os.path.exists(path):
         return G.CSRGraph.load(path)
-    g = _build(wl.graph_kind, dict(wl.graph_args))
+    args = dict(wl.graph_args)
+    if wl.graph_kind == "chung_lu":
+        args["progress"] = progress
+    g = _build(wl.graph_kind, args)
     if use_cache:
         g.save(path)
     return g

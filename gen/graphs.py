@@ -70,53 +70,58 @@ class CSRGraph:
             return CSRGraph(int(f["n"]), f["rowptr"], f["col"], w)
 
 
-def from_edges(n: int, u, v, w=None) -> CSRGraph:
+def from_edges(n: int, u, v, w=None, sorted_unique: bool = False) -> CSRGraph:
     """Build the symmetric CSR of an undirected edge list.
 
     Self-loops are rejected; repeated pairs keep the weight of their first
-    occurrence.  Rows list their lower neighbours first, then their upper ones,
-    which is ascending column order.
+    occurrence.  With ``sorted_unique`` the pairs must already satisfy u < v and be
+    strictly increasing in (u, v) order, which skips the deduplication sort.  Rows list
+    their lower neighbours first, then their upper ones, which is ascending column
+    order.
     """
-    u = np.asarray(u, dtype=np.int64)
-    v = np.asarray(v, dtype=np.int64)
-    if u.shape != v.shape:
-        raise ValueError("u and v differ in length")
-    if np.any(u == v):
-        raise ValueError("self-loops are not allowed")
-    if u.size and (min(u.min(), v.min()) < 0 or max(u.max(), v.max()) >= n):
-        raise ValueError("endpoint out of range")
-    a = np.minimum(u, v)
-    b = np.maximum(u, v)
-    key = a * np.int64(n) + b
-    key, first = np.unique(key, return_index=True)
-    a = (key // n).astype(np.int64)
-    b = (key % n).astype(np.int64)
-    if w is not None:
-        w = np.asarray(w)[first]
-    m = key.size
+    if sorted_unique:
+        a = np.asarray(u, dtype=np.int64)
+        b = np.asarray(v, dtype=np.int64)
+        if w is not None:
+            w = np.asarray(w)
+    else:
+        u = np.asarray(u, dtype=np.int64)
+        v = np.asarray(v, dtype=np.int64)
+        if u.shape != v.shape:
+            raise ValueError("u and v differ in length")
+        if np.any(u == v):
+            raise ValueError("self-loops are not allowed")
+        if u.size and (min(u.min(), v.min()) < 0 or max(u.max(), v.max()) >= n):
+            raise ValueError("endpoint out of range")
+        key = np.minimum(u, v) * np.int64(n) + np.maximum(u, v)
+        key, first = np.unique(key, return_index=True)
+        a = key // n
+        b = key % n
+        del key
+        if w is not None:
+            w = np.asarray(w)[first]
+    m = a.size
     up = np.bincount(a, minlength=n).astype(np.int64)
     lo = np.bincount(b, minlength=n).astype(np.int64)
-    deg = up + lo
     rowptr = np.zeros(n + 1, dtype=np.int64)
-    np.cumsum(deg, out=rowptr[1:])
+    np.cumsum(up + lo, out=rowptr[1:])
     col = np.empty(2 * m, dtype=np.int32)
     wcsr = None if w is None else np.empty(2 * m, dtype=w.dtype)
     # upper entries (row a, column b): edges are sorted by (a, b) already
-    upstart = np.zeros(n, dtype=np.int64)
-    np.cumsum(up[:-1], out=upstart[1:])
-    k = np.arange(m, dtype=np.int64)
-    pos_up = rowptr[a] + lo[a] + (k - upstart[a])
-    col[pos_up] = b
+    start = rowptr[:-1] + lo - np.concatenate([[0], np.cumsum(up)[:-1]])
+    pos = start[a]
+    pos += np.arange(m, dtype=np.int64)
+    col[pos] = b
+    if w is not None:
+        wcsr[pos] = w
     # lower entries (row b, column a): stable sort by b keeps a ascending per row
     perm = np.argsort(b, kind="stable")
-    bs = b[perm]
-    lostart = np.zeros(n, dtype=np.int64)
-    np.cumsum(lo[:-1], out=lostart[1:])
-    pos_lo = rowptr[bs] + (k - lostart[bs])
-    col[pos_lo] = a[perm]
+    start = rowptr[:-1] - np.concatenate([[0], np.cumsum(lo)[:-1]])
+    pos = start[b[perm]]
+    pos += np.arange(m, dtype=np.int64)
+    col[pos] = a[perm]
     if w is not None:
-        wcsr[pos_up] = w
-        wcsr[pos_lo] = w[perm]
+        wcsr[pos] = w[perm]
     return CSRGraph(int(n), rowptr, col, wcsr)
 
 
@@ -234,8 +239,9 @@ def _reweight(g: CSRGraph, rng) -> CSRGraph:
     upper = rows < g.col
     u = rows[upper]
     v = g.col[upper].astype(np.int64)
+    del rows, upper
     w = _weights(rng, u.size)
-    return from_edges(g.n, u, v, w)
+    return from_edges(g.n, u, v, w, sorted_unique=True)
 
 
 def largest_component(g: CSRGraph) -> CSRGraph:
@@ -256,60 +262,65 @@ def largest_component(g: CSRGraph) -> CSRGraph:
     u = newid[rows[upper]]
     v = newid[g.col[upper]]
     w = None if g.w is None else g.w[upper]
-    return from_edges(int(keep.sum()), u, v, w)
+    return from_edges(int(keep.sum()), u, v, w, sorted_unique=True)
 
 
 def chung_lu(n: int, gamma: float, i0: float, m_target: int, seed: int,
              weighted: bool = False, keep_largest: bool = False,
-             overdraw: float = 1.08) -> CSRGraph:
-    """Chung–Lu power-law graph with about ``m_target`` distinct edges.
+             overdraw: float = 1.06, progress=None) -> CSRGraph:
+    """Chung–Lu power-law graph with ``m_target`` distinct edges.
 
     Node i has weight (i + i0)^(-1/(gamma-1)).  Endpoints are drawn i.i.d. in
     proportion to the weights (a multinomial count per node, randomly permuted and
-    paired), self-loops dropped, repeats removed keeping first occurrences in draw
-    order, and more pairs drawn until ``m_target`` distinct edges exist; the first
-    ``m_target`` of them in draw order are kept.  Node ids are in decreasing
-    expected-degree order.
+    paired), self-loops are dropped and repeats merged; more pairs are drawn until at
+    least ``m_target`` distinct edges exist, and a uniformly random subset of exactly
+    ``m_target`` of them is kept.  Node ids are in decreasing expected-degree order.
+    ``progress`` (a callable taking a string) reports the stages of large draws.
     """
+    say = progress or (lambda msg: None)
     rng = np.random.default_rng(seed)
     wt = (np.arange(n, dtype=np.float64) + i0) ** (-1.0 / (gamma - 1.0))
     prob = wt / wt.sum()
     keys = np.empty(0, dtype=np.int64)
-    order = np.empty(0, dtype=np.int64)
-    drawn = 0
     need = m_target
-    while True:
+    rounds = 0
+    while keys.size < m_target:
         draws = int(need * overdraw) + 1024
-        cnt = rng.multinomial(2 * draws, prob)
-        ends = np.repeat(np.arange(n, dtype=np.int64), cnt)
+        ends = np.repeat(np.arange(n, dtype=np.int32), rng.multinomial(2 * draws, prob))
         rng.shuffle(ends)
         a = ends[0::2]
         b = ends[1::2]
-        del ends
-        ok = a != b
-        lo = np.minimum(a, b)[ok]
-        hi = np.maximum(a, b)[ok]
-        pos = np.arange(drawn, drawn + draws, dtype=np.int64)[ok]
-        drawn += draws
-        del a, b, ok
-        keys = np.concatenate([keys, lo * np.int64(n) + hi])
-        order = np.concatenate([order, pos])
-        del lo, hi, pos
-        keys, first = np.unique(keys, return_index=True)
-        order = order[first]
-        if keys.size >= m_target:
-            break
-        need = int((m_target - keys.size) * max(1.0, drawn / max(keys.size, 1))) + 1
-    sel = np.argsort(order, kind="stable")[:m_target]
-    keys = np.sort(keys[sel])
-    del order, sel
+        k = np.minimum(a, b).astype(np.int64)
+        k *= n
+        k += np.maximum(a, b)
+        k = k[a != b]
+        del ends, a, b
+        keys = np.unique(np.concatenate([keys, k]))
+        del k
+        rounds += 1
+        say(f"chung_lu: round {rounds}: {keys.size} distinct edges of {m_target}")
+        need = max(1024, int((m_target - keys.size) * 1.5))
+    if keys.size > m_target:
+        r = rng.random(keys.size)
+        sel = np.argpartition(r, m_target)[:m_target]
+        del r
+        sel.sort()
+        keys = keys[sel]
+        del sel
     u = keys // n
     v = keys % n
     del keys
-    g = from_edges(n, u, v)
+    say("chung_lu: building CSR")
+    if weighted and not keep_largest:
+        # same draw as _reweight: one weight per edge in (u<v) order
+        g = from_edges(n, u, v, _weights(rng, u.size), sorted_unique=True)
+        del u, v
+        return g
+    g = from_edges(n, u, v, sorted_unique=True)
     del u, v
     if keep_largest:
         g = largest_component(g)
     if weighted:
+        say("chung_lu: weights")
         g = _reweight(g, rng)
     return g

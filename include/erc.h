@@ -1,0 +1,237 @@
+/*
+ * erc.h -- C ABI of the MI355X resistance-curvature library.
+ *
+ * The library computes, on one gfx950 GPU, the ERC-LG approximation of effective
+ * resistance curvature described in "Scalable Subgraph Sampling via Resistance
+ * Curvature" (Fei, Zhou, Hao, Li):
+ *
+ *   1. Y = B^T W^{1/2} Q for streamed blocks of a K-column JL projection Q with
+ *      entries +-1/sqrt(K)                          (Section 3.1.2; Algorithm 1)
+ *   2. (L + delta I) Z = Y by column-wise CG to relative residual tol
+ *                                                   (Eq. 5; Section 3.1.3; Alg. 1)
+ *   3. R_uv += ||Z_u - Z_v||^2 per edge, block by block        (Eq. 6; Alg. 1)
+ *   4. p_u = 1 - 1/2 sum_v w_uv R_uv,  kappa_uv = 2 (p_u + p_v) / R_uv   (Eq. 2)
+ *   5. node / edge sampling probabilities                (Eqs. 7, 8; Section 3.2)
+ *
+ * Conventions shared by every call
+ *  - Every function returns an erc_status; nothing is thrown across the ABI.  On an
+ *    error, erc_last_error() returns a message (thread-local, valid until the next
+ *    call on the same thread).
+ *  - "host" pointers are ordinary CPU memory; "device" pointers are GPU memory on the
+ *    current HIP device, owned by the caller.  The library never allocates device
+ *    memory: the graph copy and the solve workspace live in caller buffers whose
+ *    sizes come from erc_graph_bytes / erc_workspace_bytes, and those buffers must
+ *    outlive every call that uses them.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).  All
+ *    device work is enqueued on it.  erc_create and erc_resistance return after the
+ *    stream has drained; the other calls are asynchronous.
+ *  - Edges are numbered canonically: edge e is the e-th pair (u, v), u < v, in
+ *    lexicographic order.  Every per-edge array (R, kappa, edge probabilities) is
+ *    indexed by that number.  The incidence matrix B has +1 at u and -1 at v.
+ *  - A handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef ERC_H
+#define ERC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ERC_OK = 0,
+  ERC_E_INVALID_ARG = 1,     /* NULL pointer, bad size, out-of-range parameter        */
+  ERC_E_INVALID_GRAPH = 2,   /* CSR not symmetric / unsorted / self-loop / bad weight  */
+  ERC_E_WORKSPACE = 3,       /* caller buffer smaller than the size query returned    */
+  ERC_E_DEVICE = 4,          /* a HIP runtime call failed                              */
+  ERC_E_NOT_CONVERGED = 5,   /* some column hit max_iter above tol (result written)    */
+  ERC_E_NUMERIC = 6,         /* CG breakdown (p.q <= 0 or non-finite), R <= 0, NaN     */
+  ERC_E_STATE = 7            /* handle used in an invalid state                        */
+} erc_status;
+
+typedef enum { ERC_F32 = 0, ERC_F64 = 1 } erc_dtype;
+
+/* Opaque host-side handle: device pointers into the caller's graph buffer plus the
+ * host-side plan (sizes, row work lists). */
+typedef struct erc_graph_s* erc_handle;
+
+/* Undirected graph as a symmetric CSR adjacency (Section 3.1.1: L = D - A = B^T W B).
+ *  n           number of nodes (0 < n < 2^31)
+ *  rowptr      host, n+1 int64, rowptr[0] = 0, non-decreasing, rowptr[n] = nnz < 2^31
+ *  col         host, nnz int32 column indices, strictly ascending within each row
+ *  w           host, nnz weights of type w_dtype, or NULL for unit weights; every
+ *              weight finite and > 0, and w_ij == w_ji exactly
+ *  w_dtype     type of w (ignored when w == NULL)
+ *  solve_dtype working precision of the CG vectors: ERC_F32 (dot products and all
+ *              accumulations are still fp64) or ERC_F64
+ * The structure must be symmetric with no self-loops and no repeated entries; each
+ * undirected edge is stored twice.  Isolated nodes are allowed. */
+typedef struct {
+  int64_t n;
+  const int64_t* rowptr;
+  const int32_t* col;
+  const void* w;
+  erc_dtype w_dtype;
+  erc_dtype solve_dtype;
+} erc_graph_desc;
+
+/* Accumulate into R instead of overwriting it (resume, column-range sharding). */
+#define ERC_ACCUMULATE 1u
+/* Time every SpMM launch with a pair of HIP events on the caller's stream and report
+ * the sum in erc_solve_info.ms_spmm / spmm_timed (adds two event records per launch). */
+#define ERC_PROFILE_SPMM 2u
+
+/* Parameters of one resistance sweep (Algorithm 1, Require line).
+ *  K_total     total projection dimension K; the JL scale is 1/sqrt(K_total) even when
+ *              only a column range is solved (1 <= K_total)
+ *  k_block     columns per CG block, the paper's batch size b (1..256 for ERC_F32,
+ *              1..128 for ERC_F64); a block is padded internally to a power of two
+ *              (>= 16 columns for ERC_F32, >= 8 for ERC_F64)
+ *  col_begin, col_end   global column range [col_begin, col_end) of the sketch to
+ *              solve, 0 <= col_begin < col_end <= K_total
+ *  delta       diagonal shift (the paper's epsilon in Eq. 5), delta > 0
+ *  tol         per-column relative residual tolerance tau (0 < tol < 1): a column
+ *              stops once ||r|| <= tol ||y|| on the recursively updated residual
+ *  max_iter    iteration cap per block (>= 1)
+ *  check_every iterations enqueued between host convergence polls (0 = default 16);
+ *              results do not depend on it
+ *  seed        projection seed
+ *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM, or 0 */
+typedef struct {
+  int32_t K_total;
+  int32_t k_block;
+  int32_t col_begin;
+  int32_t col_end;
+  double delta;
+  double tol;
+  int32_t max_iter;
+  int32_t check_every;
+  uint64_t seed;
+  uint32_t flags;
+} erc_solve_params;
+
+/* Filled by erc_resistance when non-NULL. */
+typedef struct {
+  int32_t blocks;             /* column blocks solved                                */
+  int32_t iters_max;          /* largest per-column iteration count                  */
+  int32_t cols_unconverged;   /* columns that reached max_iter above tol             */
+  int32_t breakdowns;         /* columns stopped by p.q <= 0 or a non-finite value   */
+  int64_t iters_total;        /* sum over columns of their iteration counts          */
+  int64_t launches;           /* CG iterations enqueued (per block, summed)          */
+  int64_t nonpositive;        /* entries of R that are <= 0 or not finite at the end */
+  double max_final_relres;    /* max over columns of sqrt(rho_final / rho_0)         */
+  float ms_rhs;               /* GPU time building right-hand sides                  */
+  float ms_cg;                /* GPU time in CG iterations                           */
+  float ms_accum;             /* GPU time in edge-distance accumulation              */
+  float ms_total;             /* whole call, stream time                             */
+  float ms_spmm;              /* with ERC_PROFILE_SPMM: summed SpMM kernel time      */
+  int64_t spmm_timed;         /* with ERC_PROFILE_SPMM: SpMM launches timed          */
+} erc_solve_info;
+
+/* ---- graph ---------------------------------------------------------------------- */
+
+/* Host-only validation of a graph description (no GPU needed).  On success *m_out
+ * (if non-NULL) receives the number of undirected edges.
+ * Errors: ERC_E_INVALID_ARG (NULL/size), ERC_E_INVALID_GRAPH (structure, weights). */
+erc_status erc_validate(const erc_graph_desc* desc, int64_t* m_out);
+
+/* Size in bytes of the device buffer erc_create needs for this graph (host-only). */
+erc_status erc_graph_bytes(const erc_graph_desc* desc, size_t* bytes);
+
+/* Validate and canonicalise the graph on the host, then copy the device copy of the
+ * operator (CSR, weights, per-entry edge ids, sqrt(w) per edge, work lists) into
+ * dev_mem (device, >= erc_graph_bytes bytes, 256-byte aligned) on `stream`, and wait
+ * for the copy.  The handle refers to dev_mem, which must stay allocated until
+ * erc_destroy.  (Algorithm 1: construct sparse L; store local sparse operators.) */
+erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, void* stream,
+                      erc_handle* out);
+
+erc_status erc_num_nodes(erc_handle h, int64_t* n);
+erc_status erc_num_edges(erc_handle h, int64_t* m);
+
+/* Endpoints of every canonical edge: u_dev[e] < v_dev[e] (device, m int32 each). */
+erc_status erc_edge_endpoints(erc_handle h, int32_t* u_dev, int32_t* v_dev, void* stream);
+
+/* Frees the host-side handle only (the caller frees dev_mem).  NULL is accepted. */
+erc_status erc_destroy(erc_handle h);
+
+/* ---- resistance (Algorithm 1, Eqs. 3-6) ------------------------------------------ */
+
+/* Device workspace size for blocks of k_block columns on this graph. */
+erc_status erc_workspace_bytes(erc_handle h, int32_t k_block, size_t* bytes);
+
+/* R_dev[e] (device, m fp64) = sum over the requested columns c of (Z_uc - Z_vc)^2,
+ * where Z solves (L + delta I) Z = B^T W^{1/2} Q column by column with CG
+ * (or += with ERC_ACCUMULATE).  ws_dev is device memory of >= erc_workspace_bytes
+ * bytes.  The call blocks until the stream has drained.
+ * Returns ERC_E_NOT_CONVERGED (R still written) when a column hit max_iter above tol,
+ * ERC_E_NUMERIC on a CG breakdown or when some R_e ends <= 0 or non-finite (curvature
+ * needs R_e > 0). */
+erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws_dev,
+                          size_t ws_bytes, double* R_dev, erc_solve_info* info,
+                          void* stream);
+
+/* ---- curvature and sampling (Eq. 2; Eqs. 7-8; Section 3.2) ------------------------ */
+
+/* p_dev[u] (device, n fp64) = 1 - 1/2 sum_{v in N(u)} w_uv R_uv (1 for isolated u);
+ * kappa_dev[e] (device, m fp64) = 2 (p_u + p_v) / R_e.  Asynchronous.  Each R_e should
+ * be finite and > 0 (erc_resistance reports otherwise); the outputs are the IEEE
+ * results of the formulas whatever R holds. */
+erc_status erc_curvature(erc_handle h, const double* R_dev, double* p_dev, double* kappa_dev,
+                         void* stream);
+
+/* Node probabilities (device, n fp64): q_u = sum_{v in N(u)} (kappa_uv - kappa_min) /
+ * (kappa_max - kappa_min + eta), divided by sum_u q_u; uniform over nodes of degree > 0
+ * when every q_u is 0 (Eq. 7).  Edge probabilities (device, m fp64):
+ * q_e = sqrt(max(2 kappa_max - kappa_e, 0)) + 1 divided by its sum (Eq. 8).
+ * eta > 0.  scratch_dev is device memory of >= erc_sampling_scratch_bytes bytes.
+ * Asynchronous. */
+erc_status erc_sampling_scratch_bytes(erc_handle h, size_t* bytes);
+erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
+                              void* scratch_dev, size_t scratch_bytes,
+                              double* node_prob_dev, double* edge_prob_dev, void* stream);
+
+/* ---- diagnostics ----------------------------------------------------------------- */
+
+const char* erc_status_string(erc_status s);
+const char* erc_last_error(void);
+
+/* ---- test hooks (same conventions; used by the parity tests) ---------------------- */
+
+/* Host-only self-check of the work plan erc_create would build for this graph (no GPU
+ * needed): every stored entry is covered exactly once by the SpMM plan, every upper
+ * entry (v > u) exactly once by the per-edge pieces, every index is in range and every
+ * list fits the size bounds behind erc_graph_bytes.  ERC_E_STATE names a violation. */
+erc_status erc_debug_check_plan(const erc_graph_desc* desc);
+
+/* Canonical edge id of every stored CSR entry (device, nnz int32). */
+erc_status erc_debug_edge_ids(erc_handle h, int32_t* eid_dev, void* stream);
+
+/* Right-hand sides of columns [col0, col0 + ncols) as an n x ncols row-major array in
+ * the working precision (device).  1 <= ncols <= the maximum k_block; ws_dev: >=
+ * erc_workspace_bytes(h, ncols).  Asynchronous. */
+erc_status erc_debug_rhs(erc_handle h, int32_t K_total, int32_t col0, int32_t ncols,
+                         uint64_t seed, void* Y_dev, void* ws_dev, size_t ws_bytes,
+                         void* stream);
+
+/* Y = (L + delta I) X for an n x ncols row-major X in the working precision (device).
+ * ncols must be a padded block width: a power of two in 16..256 for ERC_F32, 8..128
+ * for ERC_F64.  ws_dev: >= erc_workspace_bytes(h, ncols). */
+erc_status erc_debug_spmm(erc_handle h, double delta, int32_t ncols, const void* X_dev,
+                          void* Y_dev, void* ws_dev, size_t ws_bytes, void* stream);
+
+/* Solve one block [col0, col0 + ncols) and copy its Z (n x ncols row-major, working
+ * precision, device) out; per-column iteration counts go to iters_host (ncols int32,
+ * may be NULL).  Blocks until the stream has drained.  Same return codes as
+ * erc_resistance. */
+erc_status erc_debug_solve_block(erc_handle h, const erc_solve_params* params, int32_t col0,
+                                 int32_t ncols, void* ws_dev, size_t ws_bytes, void* Z_dev,
+                                 int32_t* iters_host, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ERC_H */

@@ -1,0 +1,130 @@
+// Internal declarations shared by the host library and the HIP kernels.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "../../include/erc.h"
+
+namespace erc {
+
+// Threads per block of every kernel (4 wavefronts of 64).
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / 64;
+// Fan-in of one level of the deterministic grid reduction tree.
+constexpr int kTreeFan = 32;
+// Largest grid a reduced kernel may use (three tree levels of 32).
+constexpr int kMaxGrid = kTreeFan * kTreeFan * kTreeFan;
+
+// Device view of the graph operator (all pointers are device memory inside the
+// caller's graph buffer).
+struct DevGraph {
+  int32_t n;
+  int64_t nnz;
+  int64_t m;
+  int weighted;              // 0: unit weights, w == nullptr
+  const int64_t* rowptr;     // n+1
+  const int32_t* col;        // nnz, ascending per row
+  const void* w;             // nnz, working precision
+  const int32_t* eid;        // nnz, canonical edge id of each entry
+  const double* sw;          // m, sqrt(w_e) rounded once from fp64(w_e)
+  const int64_t* ubase;      // n+1, id of the first edge (u, v>u) of row u
+
+  // SpMM plan: per-wave ranges over `light`, plus block-cooperative tasks for long rows
+  int32_t grid;              // blocks of the SpMM kernel
+  const int32_t* light;      // light rows, ascending
+  const int32_t* wave_lo;    // grid*4 + 1 boundaries into `light`
+  int32_t ntask;             // block tasks (task t runs on block t % grid)
+  const int32_t* task_row;
+  const int32_t* task_mega;  // -1, or index of the multi-chunk row this chunk belongs to
+  const int32_t* task_chunk; // chunk index within its row (0 for single-chunk rows)
+  const int64_t* task_beg;   // CSR range of the task
+  const int64_t* task_end;
+  int32_t nmega;
+  const int32_t* mega_nchunk;
+  const int32_t* mega_chunk0;  // first chunk slot of each multi-chunk row
+  int32_t nchunk_slots;
+
+  // Edge pieces: ranges of the upper (v > u) entries of one row, for per-edge kernels
+  int64_t npiece;
+  const int32_t* piece_row;
+  const int64_t* piece_beg;  // CSR position
+  const int64_t* piece_end;
+};
+
+// Per-column CG state of one block, in the workspace.
+struct ColState {
+  double* rho;      // current r.r (fp64)
+  double* rho0;     // r.r of the right-hand side
+  double* thr;      // tol^2 * rho0
+  double* alpha;    // step of the current iteration
+  double* beta;     // direction update of the current iteration
+  int32_t* active;  // 1 while the column iterates
+  int32_t* iters;   // iterations taken
+  int32_t* status;  // 0 ok, 1 breakdown
+  int32_t* n_active;  // one int: number of active columns (polled by the host)
+  int32_t* one;       // one int holding 1 (keeps debug launches from exiting early)
+};
+
+// Reduction scratch for one kernel family: level buffers and tickets.
+struct Tree {
+  double* lvl0;     // grid * nval
+  double* lvl1;     // ceil(grid/32) * nval
+  double* lvl2;     // ceil(grid/1024) * nval
+  uint32_t* tick;   // ceil(grid/32) + ceil(grid/1024) + 1 counters, zero between launches
+};
+
+// Workspace of one column block of padded width kb.
+struct Work {
+  int kb;            // padded width
+  void* z;           // n x kb
+  void* r;
+  void* p;
+  void* q;
+  void* chunkbuf;    // nchunk_slots x kb partial sums of multi-chunk rows
+  double* mega_dots; // nmega x 3 x kb compensated (s, c) pairs
+  uint32_t* mega_tick;  // nmega counters
+  ColState cs;
+  Tree tree;
+  double* out;       // small fp64 output area (totals for the host, kb * 4)
+  int32_t grid_rhs, grid_upd, grid_ed;
+};
+
+// Launchers (erc_kernels.hip).  All return hipSuccess or the launch error.
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t count, hipStream_t s);
+hipError_t launch_fill_f64(double* p, double v, int64_t count, hipStream_t s);
+hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int col0, int ncols,
+                      uint64_t base, double inv_sqrt_k, double tol, hipStream_t s);
+hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double delta,
+                       const void* p, const void* r, void* q, const int32_t* gate,
+                       hipStream_t s);
+hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStream_t s);
+hipError_t launch_edge_dist(const DevGraph& g, const Work& w, erc_dtype dt, double* R,
+                            int accumulate, hipStream_t s);
+hipError_t launch_count_bad(const double* x, int64_t count, const Work& w, hipStream_t s);
+hipError_t launch_copy_cols(const DevGraph& g, const void* src, int kb, erc_dtype dt, int ncols,
+                            void* dst, hipStream_t s);
+hipError_t launch_node_p(const DevGraph& g, erc_dtype dt, const double* R, double* p,
+                         hipStream_t s);
+hipError_t launch_edge_kappa(const DevGraph& g, const double* R, const double* p, double* kappa,
+                             hipStream_t s);
+hipError_t launch_endpoints(const DevGraph& g, int32_t* u, int32_t* v, hipStream_t s);
+hipError_t launch_eids(const DevGraph& g, int32_t* out, hipStream_t s);
+
+struct SampleWork {
+  Tree tree;
+  double* totals;    // [0] -kappa_min, [1] kappa_max, [2] node sum, [3] edge sum, [4] bad count
+  int32_t grid;
+};
+hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,
+                           const SampleWork& sw, double* pn, double* pe, hipStream_t s);
+
+// Tree sizing helpers (host).
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t tree_ticks(int grid) {
+  return ceil_div(grid, kTreeFan) + ceil_div(grid, kTreeFan * kTreeFan) + 1;
+}
+
+}  // namespace erc

@@ -1,0 +1,1085 @@
+// Host side of the resistance-curvature library: graph validation and canonical edge
+// numbering, the device work plan, buffer layouts, and the column-block CG driver of
+// Algorithm 1 (streamed right-hand sides, batched CG, edge-block accumulation).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "erc_common.h"
+
+using namespace erc;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+erc_status fail(erc_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+#define ERC_HIP(call)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (call);                                                            \
+    if (e_ != hipSuccess)                                                              \
+      return fail(ERC_E_DEVICE, std::string(#call) + ": " + hipGetErrorString(e_));   \
+  } while (0)
+
+// Per-row cost of the SpMM plan, in units of one neighbour.
+constexpr double kRowCost = 8.0;
+// Largest SpMM grid (blocks of 4 waves).
+constexpr int kMaxSpmmGrid = 8192;
+// Longest edge piece of the per-edge kernels.
+constexpr int64_t kPiece = 1024;
+// Grid caps of the other kernels.
+constexpr int kMaxGridRhs = 8192;
+constexpr int kMaxGridUpd = 8192;
+constexpr int kMaxGridEd = 8192;
+constexpr int kCountBadGrid = 2048;
+constexpr int kSampleGrid = 2048;
+constexpr int kDefaultCheck = 16;
+
+size_t dsize(erc_dtype t) { return t == ERC_F32 ? 4 : 8; }
+int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+// Sizes that depend only on (n, nnz): the plan shape and upper bounds of its lists.
+struct Shape {
+  int64_t n, nnz, m;
+  double share;      // target cost per wave
+  int waves, grid;   // SpMM wavefronts and blocks
+  int64_t heavy;     // rows with degree above this are block tasks
+  int64_t chunk;     // block tasks are at most this long
+  int64_t ntask_max, nmega_max, nslot_max, npiece_max;
+};
+
+Shape make_shape(int64_t n, int64_t nnz) {
+  Shape s{};
+  s.n = n;
+  s.nnz = nnz;
+  s.m = nnz / 2;
+  const double total = static_cast<double>(nnz) + kRowCost * static_cast<double>(n);
+  s.share = std::max(64.0, total / (kMaxSpmmGrid * kWavesPerBlock));
+  int64_t waves = static_cast<int64_t>(std::ceil(total / s.share));
+  waves = std::max<int64_t>(kWavesPerBlock, align_up(waves, kWavesPerBlock));
+  waves = std::min<int64_t>(waves, static_cast<int64_t>(kMaxSpmmGrid) * kWavesPerBlock);
+  s.waves = static_cast<int>(waves);
+  s.grid = s.waves / kWavesPerBlock;
+  s.heavy = std::max<int64_t>(256, static_cast<int64_t>(2.0 * s.share));
+  s.chunk = std::max<int64_t>(1024, static_cast<int64_t>(8.0 * s.share));
+  s.ntask_max = nnz / s.heavy + nnz / s.chunk + 1;
+  s.nmega_max = nnz / s.chunk + 1;
+  s.nslot_max = 2 * (nnz / s.chunk) + 1;
+  s.npiece_max = n + s.m / kPiece + 1;
+  return s;
+}
+
+// Byte layout of the graph buffer.
+struct GraphLayout {
+  int64_t rowptr, col, w, eid, sw, ubase, light, wave_lo, task_row, task_mega, task_chunk,
+      task_beg, task_end, mega_nchunk, mega_chunk0, piece_row, piece_beg, piece_end, total;
+};
+
+GraphLayout graph_layout(const Shape& s, bool weighted, erc_dtype dt) {
+  GraphLayout L{};
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off = align_up(off + std::max<int64_t>(bytes, 0), 256);
+    return at;
+  };
+  L.rowptr = take((s.n + 1) * 8);
+  L.col = take(s.nnz * 4);
+  L.w = take(weighted ? s.nnz * static_cast<int64_t>(dsize(dt)) : 0);
+  L.eid = take(s.nnz * 4);
+  L.sw = take(s.m * 8);
+  L.ubase = take((s.n + 1) * 8);
+  L.light = take(s.n * 4);
+  L.wave_lo = take((static_cast<int64_t>(s.waves) + 1) * 4);
+  L.task_row = take(s.ntask_max * 4);
+  L.task_mega = take(s.ntask_max * 4);
+  L.task_chunk = take(s.ntask_max * 4);
+  L.task_beg = take(s.ntask_max * 8);
+  L.task_end = take(s.ntask_max * 8);
+  L.mega_nchunk = take(s.nmega_max * 4);
+  L.mega_chunk0 = take(s.nmega_max * 4);
+  L.piece_row = take(s.npiece_max * 4);
+  L.piece_beg = take(s.npiece_max * 8);
+  L.piece_end = take(s.npiece_max * 8);
+  L.total = off;
+  return L;
+}
+
+erc_status check_desc(const erc_graph_desc* d) {
+  if (d == nullptr) return fail(ERC_E_INVALID_ARG, "graph description is NULL");
+  if (d->n <= 0 || d->n >= (int64_t(1) << 31))
+    return fail(ERC_E_INVALID_ARG, "n must be in [1, 2^31)");
+  if (d->rowptr == nullptr) return fail(ERC_E_INVALID_ARG, "rowptr is NULL");
+  if (d->solve_dtype != ERC_F32 && d->solve_dtype != ERC_F64)
+    return fail(ERC_E_INVALID_ARG, "solve_dtype must be ERC_F32 or ERC_F64");
+  if (d->w != nullptr && d->w_dtype != ERC_F32 && d->w_dtype != ERC_F64)
+    return fail(ERC_E_INVALID_ARG, "w_dtype must be ERC_F32 or ERC_F64");
+  const int64_t nnz = d->rowptr[d->n];
+  if (d->rowptr[0] != 0) return fail(ERC_E_INVALID_GRAPH, "rowptr[0] must be 0");
+  if (nnz < 0 || nnz >= (int64_t(1) << 31))
+    return fail(ERC_E_INVALID_GRAPH, "nnz must be in [0, 2^31)");
+  if (nnz > 0 && d->col == nullptr) return fail(ERC_E_INVALID_ARG, "col is NULL");
+  return ERC_OK;
+}
+
+// Canonical form of a validated graph.
+struct Canon {
+  int64_t m = 0;
+  std::vector<int32_t> eid;    // nnz
+  std::vector<double> sw;      // m
+  std::vector<int64_t> ubase;  // n+1
+  std::vector<unsigned char> wstore;  // nnz weights in the working precision
+};
+
+template <typename WT>
+erc_status sweep(const erc_graph_desc* d, const WT* w, Canon* out) {
+  const int64_t n = d->n;
+  const int64_t* rp = d->rowptr;
+  const int32_t* col = d->col;
+  const int64_t nnz = rp[n];
+  for (int64_t i = 0; i < n; ++i)
+    if (rp[i + 1] < rp[i]) return fail(ERC_E_INVALID_GRAPH, "rowptr decreases at row " + std::to_string(i));
+  if (nnz % 2 != 0) return fail(ERC_E_INVALID_GRAPH, "odd number of stored entries: not symmetric");
+  std::vector<int64_t> cursor(n, 0);
+  if (out) {
+    out->eid.assign(nnz, -1);
+    out->sw.assign(nnz / 2, 0.0);
+    out->ubase.assign(n + 1, 0);
+  }
+  int64_t next_edge = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (out) out->ubase[i] = next_edge;
+    for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) {
+      const int64_t j = col[pos];
+      if (j < 0 || j >= n)
+        return fail(ERC_E_INVALID_GRAPH, "column index out of range in row " + std::to_string(i));
+      if (j == i) return fail(ERC_E_INVALID_GRAPH, "self-loop at node " + std::to_string(i));
+      if (pos > rp[i] && col[pos - 1] >= j)
+        return fail(ERC_E_INVALID_GRAPH,
+                    "columns not strictly ascending in row " + std::to_string(i));
+      // the i-th node to list j must be j's next stored neighbour
+      const int64_t tpos = rp[j] + cursor[j]++;
+      if (tpos >= rp[j + 1] || col[tpos] != i)
+        return fail(ERC_E_INVALID_GRAPH, "structure is not symmetric at entry (" +
+                                             std::to_string(i) + ", " + std::to_string(j) + ")");
+      if (w != nullptr) {
+        const WT x = w[pos];
+        if (!(std::isfinite(static_cast<double>(x)) && x > WT(0)))
+          return fail(ERC_E_INVALID_GRAPH, "weight must be finite and > 0 at entry (" +
+                                               std::to_string(i) + ", " + std::to_string(j) + ")");
+        if (!(w[tpos] == x))
+          return fail(ERC_E_INVALID_GRAPH, "weights not symmetric at entry (" +
+                                               std::to_string(i) + ", " + std::to_string(j) + ")");
+      }
+      if (i < j) {
+        if (out) {
+          out->eid[pos] = static_cast<int32_t>(next_edge);
+          out->eid[tpos] = static_cast<int32_t>(next_edge);
+          out->sw[next_edge] = (w != nullptr) ? std::sqrt(static_cast<double>(w[pos])) : 1.0;
+        }
+        ++next_edge;
+      }
+    }
+  }
+  if (out) {
+    out->ubase[n] = next_edge;
+    out->m = next_edge;
+  }
+  if (next_edge * 2 != nnz) return fail(ERC_E_INVALID_GRAPH, "structure is not symmetric");
+  return ERC_OK;
+}
+
+erc_status canonicalise(const erc_graph_desc* d, Canon* out) {
+  erc_status st = check_desc(d);
+  if (st != ERC_OK) return st;
+  if (d->w == nullptr) return sweep<float>(d, nullptr, out);
+  if (d->w_dtype == ERC_F32) return sweep<float>(d, static_cast<const float*>(d->w), out);
+  return sweep<double>(d, static_cast<const double*>(d->w), out);
+}
+
+// Host copy of the work plan.
+struct Plan {
+  std::vector<int32_t> light, wave_lo;
+  std::vector<int32_t> task_row, task_mega, task_chunk;
+  std::vector<int64_t> task_beg, task_end;
+  std::vector<int32_t> mega_nchunk, mega_chunk0;
+  int32_t nslot = 0;
+  std::vector<int32_t> piece_row;
+  std::vector<int64_t> piece_beg, piece_end;
+};
+
+void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P) {
+  const int64_t n = d->n;
+  const int64_t* rp = d->rowptr;
+  // long rows -> block tasks, longest first; very long rows are split into chunks
+  std::vector<int32_t> heavy;
+  for (int64_t i = 0; i < n; ++i)
+    if (rp[i + 1] - rp[i] > s.heavy) heavy.push_back(static_cast<int32_t>(i));
+  std::stable_sort(heavy.begin(), heavy.end(), [&](int32_t a, int32_t b) {
+    return (rp[a + 1] - rp[a]) > (rp[b + 1] - rp[b]);
+  });
+  struct Task { int32_t row, mega, chunk; int64_t beg, end; };
+  std::vector<Task> tasks;
+  for (int32_t i : heavy) {
+    const int64_t b = rp[i], e = rp[i + 1];
+    const int64_t nch = (e - b + s.chunk - 1) / s.chunk;
+    if (nch == 1) {
+      tasks.push_back({i, -1, 0, b, e});
+    } else {
+      const int32_t mh = static_cast<int32_t>(P->mega_nchunk.size());
+      P->mega_nchunk.push_back(static_cast<int32_t>(nch));
+      P->mega_chunk0.push_back(P->nslot);
+      P->nslot += static_cast<int32_t>(nch);
+      for (int64_t k = 0; k < nch; ++k)
+        tasks.push_back({i, mh, static_cast<int32_t>(k), b + k * s.chunk, std::min(e, b + (k + 1) * s.chunk)});
+    }
+  }
+  std::stable_sort(tasks.begin(), tasks.end(), [](const Task& a, const Task& b) {
+    return (a.end - a.beg) > (b.end - b.beg);
+  });
+  std::vector<double> hcost(s.grid, 0.0);
+  for (size_t t = 0; t < tasks.size(); ++t) {
+    P->task_row.push_back(tasks[t].row);
+    P->task_mega.push_back(tasks[t].mega);
+    P->task_chunk.push_back(tasks[t].chunk);
+    P->task_beg.push_back(tasks[t].beg);
+    P->task_end.push_back(tasks[t].end);
+    hcost[t % s.grid] += static_cast<double>(tasks[t].end - tasks[t].beg) + kRowCost;
+  }
+  // short rows -> contiguous per-wave ranges balanced by cost, leaving room for tasks
+  double light_total = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t dg = rp[i + 1] - rp[i];
+    if (dg <= s.heavy) {
+      P->light.push_back(static_cast<int32_t>(i));
+      light_total += static_cast<double>(dg) + kRowCost;
+    }
+  }
+  const int W = s.waves;
+  std::vector<double> budget(W);
+  double bsum = 0.0;
+  for (int w = 0; w < W; ++w) {
+    budget[w] = std::max(0.0, s.share - hcost[w / kWavesPerBlock] / kWavesPerBlock);
+    bsum += budget[w];
+  }
+  for (int w = 0; w < W; ++w)
+    budget[w] = bsum > 0.0 ? budget[w] * (light_total / bsum) : light_total / W;
+  P->wave_lo.assign(W + 1, 0);
+  const int64_t nl = static_cast<int64_t>(P->light.size());
+  int w = 0;
+  double cum = 0.0, tnext = budget[0];
+  for (int64_t k = 0; k < nl; ++k) {
+    const int32_t i = P->light[k];
+    const double cost = static_cast<double>(rp[i + 1] - rp[i]) + kRowCost;
+    const double mid = cum + 0.5 * cost;
+    while (w < W - 1 && mid >= tnext) {
+      ++w;
+      P->wave_lo[w] = static_cast<int32_t>(k);
+      tnext += budget[w];
+    }
+    cum += cost;
+  }
+  while (w < W - 1) P->wave_lo[++w] = static_cast<int32_t>(nl);
+  P->wave_lo[W] = static_cast<int32_t>(nl);
+  // edge pieces over the upper entries of each row
+  for (int64_t u = 0; u < n; ++u) {
+    const int64_t up = c.ubase[u + 1] - c.ubase[u];
+    const int64_t upos = rp[u + 1] - up;
+    for (int64_t b = upos; b < rp[u + 1]; b += kPiece) {
+      P->piece_row.push_back(static_cast<int32_t>(u));
+      P->piece_beg.push_back(b);
+      P->piece_end.push_back(std::min(rp[u + 1], b + kPiece));
+    }
+  }
+}
+
+// Workspace layout for a padded block width.
+struct WorkLayout {
+  int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rho0, thr, alpha, beta, active,
+      iters, status, n_active, one, lvl0, lvl1, lvl2, tick, out, total;
+  int grid_rhs, grid_upd, grid_ed, grid_tree;
+};
+
+int padded_width(erc_dtype dt, int k) {
+  int kb = (dt == ERC_F32) ? 16 : 8;
+  while (kb < k) kb <<= 1;
+  return kb;
+}
+int max_width(erc_dtype dt) { return dt == ERC_F32 ? 256 : 128; }
+
+}  // namespace
+
+struct erc_graph_s {
+  int64_t n = 0, nnz = 0, m = 0;
+  erc_dtype dt = ERC_F32;
+  bool weighted = false;
+  int device = 0;
+  int64_t nonisolated = 0;
+  Shape shape{};
+  DevGraph dg{};
+  int32_t* pinned = nullptr;  // host poll slots and per-column readback
+  hipEvent_t ev[6] = {};
+  std::vector<hipEvent_t> prof;  // SpMM timing pairs: [slot][launch][begin/end]
+  int prof_check = 0;
+};
+
+namespace {
+
+constexpr int kPinnedInts = 4096;
+
+WorkLayout work_layout(const erc_graph_s* h, int kb) {
+  WorkLayout L{};
+  const int64_t s = static_cast<int64_t>(dsize(h->dt));
+  const int vec = h->dt == ERC_F32 ? 4 : 2;
+  L.grid_rhs = static_cast<int>(std::min<int64_t>(kMaxGridRhs, std::max<int64_t>(1, ceil_div(h->n, kWavesPerBlock))));
+  const int64_t nvec = h->n * kb / vec;
+  L.grid_upd = static_cast<int>(std::min<int64_t>(kMaxGridUpd, std::max<int64_t>(1, ceil_div(nvec, kBlock * 4))));
+  L.grid_ed = static_cast<int>(std::min<int64_t>(kMaxGridEd, std::max<int64_t>(1, ceil_div(h->dg.npiece, kWavesPerBlock))));
+  L.grid_tree = std::max({h->dg.grid, L.grid_rhs, L.grid_upd, kCountBadGrid});
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off = align_up(off + std::max<int64_t>(bytes, 0), 256);
+    return at;
+  };
+  const int64_t vecb = h->n * kb * s;
+  L.z = take(vecb);
+  L.r = take(vecb);
+  L.p = take(vecb);
+  L.q = take(vecb);
+  L.chunkbuf = take(static_cast<int64_t>(h->dg.nchunk_slots) * kb * s);
+  L.mega_dots = take(static_cast<int64_t>(h->dg.nmega) * 3 * kb * 16);
+  L.mega_tick = take(static_cast<int64_t>(h->dg.nmega) * 4);
+  L.rho = take(kb * 8);
+  L.rho0 = take(kb * 8);
+  L.thr = take(kb * 8);
+  L.alpha = take(kb * 8);
+  L.beta = take(kb * 8);
+  L.active = take(kb * 4);
+  L.iters = take(kb * 4);
+  L.status = take(kb * 4);
+  L.n_active = take(4);
+  L.one = take(4);
+  const int64_t nval = 6 * kb;  // three compensated (s, c) pairs per column
+  L.lvl0 = take(static_cast<int64_t>(L.grid_tree) * nval * 8);
+  L.lvl1 = take(ceil_div(L.grid_tree, kTreeFan) * nval * 8);
+  L.lvl2 = take(ceil_div(L.grid_tree, kTreeFan * kTreeFan) * nval * 8);
+  L.tick = take(tree_ticks(L.grid_tree) * 4);
+  L.out = take(8 * 8);
+  L.total = off;
+  return L;
+}
+
+Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
+  char* b = static_cast<char*>(ws);
+  Work w{};
+  w.kb = kb;
+  w.z = b + L.z;
+  w.r = b + L.r;
+  w.p = b + L.p;
+  w.q = b + L.q;
+  w.chunkbuf = b + L.chunkbuf;
+  w.mega_dots = reinterpret_cast<double*>(b + L.mega_dots);
+  w.mega_tick = reinterpret_cast<uint32_t*>(b + L.mega_tick);
+  w.cs.rho = reinterpret_cast<double*>(b + L.rho);
+  w.cs.rho0 = reinterpret_cast<double*>(b + L.rho0);
+  w.cs.thr = reinterpret_cast<double*>(b + L.thr);
+  w.cs.alpha = reinterpret_cast<double*>(b + L.alpha);
+  w.cs.beta = reinterpret_cast<double*>(b + L.beta);
+  w.cs.active = reinterpret_cast<int32_t*>(b + L.active);
+  w.cs.iters = reinterpret_cast<int32_t*>(b + L.iters);
+  w.cs.status = reinterpret_cast<int32_t*>(b + L.status);
+  w.cs.n_active = reinterpret_cast<int32_t*>(b + L.n_active);
+  w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
+  w.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
+  w.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
+  w.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
+  w.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
+  w.out = reinterpret_cast<double*>(b + L.out);
+  w.grid_rhs = L.grid_rhs;
+  w.grid_upd = L.grid_upd;
+  w.grid_ed = L.grid_ed;
+  return w;
+}
+
+// Zero the tickets and set the constant-one gate (fill kernels, so a captured stream
+// records no memset node).
+erc_status prepare_work(const erc_graph_s* h, const Work& w, const WorkLayout& L, hipStream_t s) {
+  ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(L.grid_tree), s));
+  ERC_HIP(launch_fill_u32(w.mega_tick, 0u, h->dg.nmega, s));
+  ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.one), 1u, 1, s));
+  return ERC_OK;
+}
+
+uint64_t splitmix_first(uint64_t seed) {
+  uint64_t z = seed + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+erc_status check_params(const erc_graph_s* h, const erc_solve_params* p) {
+  if (p == nullptr) return fail(ERC_E_INVALID_ARG, "params is NULL");
+  if (p->K_total < 1) return fail(ERC_E_INVALID_ARG, "K_total must be >= 1");
+  if (p->k_block < 1 || p->k_block > max_width(h->dt))
+    return fail(ERC_E_INVALID_ARG, "k_block out of range for the working precision");
+  if (p->col_begin < 0 || p->col_begin >= p->col_end || p->col_end > p->K_total)
+    return fail(ERC_E_INVALID_ARG, "column range must satisfy 0 <= begin < end <= K_total");
+  if (!(p->delta > 0.0) || !std::isfinite(p->delta))
+    return fail(ERC_E_INVALID_ARG, "delta must be finite and > 0");
+  if (!(p->tol > 0.0 && p->tol < 1.0)) return fail(ERC_E_INVALID_ARG, "tol must be in (0, 1)");
+  if (p->max_iter < 1) return fail(ERC_E_INVALID_ARG, "max_iter must be >= 1");
+  if (p->check_every < 0) return fail(ERC_E_INVALID_ARG, "check_every must be >= 0");
+  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM)) != 0u)
+    return fail(ERC_E_INVALID_ARG, "unknown flag");
+  return ERC_OK;
+}
+
+struct BlockStats {
+  int32_t iters_max = 0, unconverged = 0, breakdowns = 0;
+  int64_t iters_total = 0, launches = 0;
+  double max_relres = 0.0;
+  float ms_rhs = 0, ms_cg = 0, ms_accum = 0, ms_spmm = 0;
+  int64_t spmm_timed = 0;
+};
+
+erc_status ensure_prof_events(erc_graph_s* h, int check) {
+  if (h->prof_check >= check) return ERC_OK;
+  for (auto& e : h->prof)
+    if (e) hipEventDestroy(e);
+  h->prof.assign(static_cast<size_t>(4) * check, nullptr);
+  for (auto& e : h->prof) ERC_HIP(hipEventCreate(&e));
+  h->prof_check = check;
+  return ERC_OK;
+}
+
+// Sum the SpMM event pairs of one poll group.
+erc_status read_prof(erc_graph_s* h, int slot, int count, BlockStats* st) {
+  for (int j = 0; j < count; ++j) {
+    float ms = 0.0f;
+    hipEvent_t* pr = &h->prof[(static_cast<size_t>(slot) * h->prof_check + j) * 2];
+    ERC_HIP(hipEventElapsedTime(&ms, pr[0], pr[1]));
+    st->ms_spmm += ms;
+    st->spmm_timed += 1;
+  }
+  return ERC_OK;
+}
+
+// One column block: right-hand sides, CG to tol or max_iter, then (if R != nullptr)
+// the edge-distance accumulation.  Ends with the stream drained.
+erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w, int col0, int nc,
+                       double* R, int accumulate, int32_t* iters_out, BlockStats* st,
+                       hipStream_t s) {
+  const double inv_sqrt_k = 1.0 / std::sqrt(static_cast<double>(p->K_total));
+  const uint64_t base = splitmix_first(p->seed);
+  ERC_HIP(hipEventRecord(h->ev[0], s));
+  ERC_HIP(launch_rhs(h->dg, w, h->dt, p->K_total, col0, nc, base, inv_sqrt_k, p->tol, s));
+  ERC_HIP(hipEventRecord(h->ev[1], s));
+  const int check = p->check_every > 0 ? p->check_every : kDefaultCheck;
+  const bool prof = (p->flags & ERC_PROFILE_SPMM) != 0u;
+  if (prof) {
+    erc_status pst = ensure_prof_events(h, check);
+    if (pst != ERC_OK) return pst;
+  }
+  volatile int32_t* poll = h->pinned;
+  int done = 0, pending = -1, slot = 0;
+  int group_count[2] = {0, 0};
+  bool stop = false;
+  while (!stop && done < p->max_iter) {
+    const int nb = std::min(check, p->max_iter - done);
+    slot ^= 1;
+    for (int j = 0; j < nb; ++j) {
+      hipEvent_t* pr = prof ? &h->prof[(static_cast<size_t>(slot) * h->prof_check + j) * 2] : nullptr;
+      if (prof) ERC_HIP(hipEventRecord(pr[0], s));
+      ERC_HIP(launch_spmm(h->dg, w, h->dt, p->delta, w.p, w.r, w.q, w.cs.n_active, s));
+      if (prof) ERC_HIP(hipEventRecord(pr[1], s));
+      ERC_HIP(launch_update(h->dg, w, h->dt, s));
+    }
+    group_count[slot] = nb;
+    done += nb;
+    st->launches += nb;
+    ERC_HIP(hipMemcpyAsync(const_cast<int32_t*>(poll) + slot, w.cs.n_active, sizeof(int32_t),
+                           hipMemcpyDeviceToHost, s));
+    ERC_HIP(hipEventRecord(h->ev[4 + slot], s));
+    if (pending >= 0) {
+      ERC_HIP(hipEventSynchronize(h->ev[4 + pending]));
+      if (poll[pending] == 0) stop = true;
+      if (prof) {
+        erc_status pst = read_prof(h, pending, group_count[pending], st);
+        if (pst != ERC_OK) return pst;
+        group_count[pending] = 0;
+      }
+    }
+    pending = slot;
+  }
+  ERC_HIP(hipEventRecord(h->ev[2], s));
+  if (R != nullptr) ERC_HIP(launch_edge_dist(h->dg, w, h->dt, R, accumulate, s));
+  ERC_HIP(hipEventRecord(h->ev[3], s));
+  // per-column state back to the host
+  const int kb = w.kb;
+  int32_t* hb = h->pinned + 8;
+  ERC_HIP(hipMemcpyAsync(hb, w.cs.iters, kb * 4, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(hb + kb, w.cs.active, kb * 4, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(hb + 2 * kb, w.cs.status, kb * 4, hipMemcpyDeviceToHost, s));
+  double* hd = reinterpret_cast<double*>(h->pinned + 8 + 4 * kb);
+  ERC_HIP(hipMemcpyAsync(hd, w.cs.rho, kb * 8, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(hd + kb, w.cs.rho0, kb * 8, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipStreamSynchronize(s));
+  if (prof && pending >= 0 && group_count[pending] > 0) {
+    erc_status pst = read_prof(h, pending, group_count[pending], st);
+    if (pst != ERC_OK) return pst;
+  }
+  for (int c = 0; c < nc; ++c) {
+    const int32_t it = hb[c];
+    st->iters_total += it;
+    st->iters_max = std::max(st->iters_max, it);
+    if (hb[2 * kb + c] != 0) st->breakdowns += 1;
+    else if (hb[kb + c] != 0) st->unconverged += 1;
+    if (hd[kb + c] > 0.0) st->max_relres = std::max(st->max_relres, std::sqrt(hd[c] / hd[kb + c]));
+    if (iters_out) iters_out[c] = it;
+  }
+  float a = 0, b = 0, c = 0;
+  ERC_HIP(hipEventElapsedTime(&a, h->ev[0], h->ev[1]));
+  ERC_HIP(hipEventElapsedTime(&b, h->ev[1], h->ev[2]));
+  ERC_HIP(hipEventElapsedTime(&c, h->ev[2], h->ev[3]));
+  st->ms_rhs += a;
+  st->ms_cg += b;
+  st->ms_accum += c;
+  return ERC_OK;
+}
+
+erc_status check_handle(const erc_graph_s* h) {
+  if (h == nullptr) return fail(ERC_E_INVALID_ARG, "handle is NULL");
+  return ERC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* erc_status_string(erc_status s) {
+  switch (s) {
+    case ERC_OK: return "ok";
+    case ERC_E_INVALID_ARG: return "invalid argument";
+    case ERC_E_INVALID_GRAPH: return "invalid graph";
+    case ERC_E_WORKSPACE: return "workspace too small";
+    case ERC_E_DEVICE: return "device error";
+    case ERC_E_NOT_CONVERGED: return "not converged";
+    case ERC_E_NUMERIC: return "numerical breakdown";
+    case ERC_E_STATE: return "invalid state";
+  }
+  return "unknown status";
+}
+
+const char* erc_last_error(void) { return g_last_error.c_str(); }
+
+erc_status erc_validate(const erc_graph_desc* desc, int64_t* m_out) {
+  g_last_error.clear();
+  erc_status st = check_desc(desc);
+  if (st != ERC_OK) return st;
+  Canon c;
+  if (desc->w == nullptr) st = sweep<float>(desc, nullptr, nullptr);
+  else if (desc->w_dtype == ERC_F32) st = sweep<float>(desc, static_cast<const float*>(desc->w), nullptr);
+  else st = sweep<double>(desc, static_cast<const double*>(desc->w), nullptr);
+  if (st != ERC_OK) return st;
+  if (m_out) *m_out = desc->rowptr[desc->n] / 2;
+  return ERC_OK;
+}
+
+erc_status erc_graph_bytes(const erc_graph_desc* desc, size_t* bytes) {
+  g_last_error.clear();
+  erc_status st = check_desc(desc);
+  if (st != ERC_OK) return st;
+  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+  const Shape s = make_shape(desc->n, desc->rowptr[desc->n]);
+  *bytes = static_cast<size_t>(graph_layout(s, desc->w != nullptr, desc->solve_dtype).total);
+  return ERC_OK;
+}
+
+erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, void* stream,
+                      erc_handle* out) {
+  g_last_error.clear();
+  if (out == nullptr) return fail(ERC_E_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (dev_mem == nullptr) return fail(ERC_E_INVALID_ARG, "dev_mem is NULL");
+  if (reinterpret_cast<uintptr_t>(dev_mem) % 256 != 0)
+    return fail(ERC_E_INVALID_ARG, "dev_mem must be 256-byte aligned");
+  Canon c;
+  erc_status st = canonicalise(desc, &c);
+  if (st != ERC_OK) return st;
+  const int64_t n = desc->n;
+  const int64_t nnz = desc->rowptr[n];
+  const Shape s = make_shape(n, nnz);
+  const bool weighted = desc->w != nullptr;
+  const GraphLayout L = graph_layout(s, weighted, desc->solve_dtype);
+  if (static_cast<int64_t>(bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "graph buffer smaller than erc_graph_bytes");
+  Plan P;
+  build_plan(desc, c, s, &P);
+  if (static_cast<int64_t>(P.task_row.size()) > s.ntask_max ||
+      static_cast<int64_t>(P.mega_nchunk.size()) > s.nmega_max ||
+      static_cast<int64_t>(P.piece_row.size()) > s.npiece_max || P.nslot > s.nslot_max)
+    return fail(ERC_E_STATE, "internal: work plan exceeds its size bound");
+  // weights in the working precision
+  std::vector<float> wf;
+  std::vector<double> wd;
+  const void* wsrc = nullptr;
+  if (weighted) {
+    if (desc->solve_dtype == ERC_F32) {
+      if (desc->w_dtype == ERC_F32) {
+        wsrc = desc->w;
+      } else {
+        wf.resize(nnz);
+        const double* x = static_cast<const double*>(desc->w);
+        for (int64_t k = 0; k < nnz; ++k) wf[k] = static_cast<float>(x[k]);
+        wsrc = wf.data();
+      }
+    } else {
+      if (desc->w_dtype == ERC_F64) {
+        wsrc = desc->w;
+      } else {
+        wd.resize(nnz);
+        const float* x = static_cast<const float*>(desc->w);
+        for (int64_t k = 0; k < nnz; ++k) wd[k] = static_cast<double>(x[k]);
+        wsrc = wd.data();
+      }
+    }
+  }
+  auto* h = new erc_graph_s();
+  h->n = n;
+  h->nnz = nnz;
+  h->m = c.m;
+  h->dt = desc->solve_dtype;
+  h->weighted = weighted;
+  h->shape = s;
+  for (int64_t i = 0; i < n; ++i) h->nonisolated += desc->rowptr[i + 1] > desc->rowptr[i];
+  auto cleanup = [&](erc_status e) {
+    if (h->pinned) hipHostFree(h->pinned);
+    for (auto& ev : h->ev)
+      if (ev) hipEventDestroy(ev);
+    delete h;
+    return e;
+  };
+  if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipGetDevice failed"));
+  if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), kPinnedInts * sizeof(int32_t),
+                    hipHostMallocDefault) != hipSuccess)
+    return cleanup(fail(ERC_E_DEVICE, "hipHostMalloc failed"));
+  for (auto& ev : h->ev)
+    if (hipEventCreate(&ev) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipEventCreate failed"));
+  char* base = static_cast<char*>(dev_mem);
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  auto up = [&](int64_t off, const void* src, int64_t nbytes) -> hipError_t {
+    if (nbytes <= 0) return hipSuccess;
+    return hipMemcpyAsync(base + off, src, nbytes, hipMemcpyHostToDevice, hs);
+  };
+  hipError_t e = hipSuccess;
+  auto chk = [&](hipError_t x) { if (e == hipSuccess) e = x; };
+  chk(up(L.rowptr, desc->rowptr, (n + 1) * 8));
+  chk(up(L.col, desc->col, nnz * 4));
+  if (weighted) chk(up(L.w, wsrc, nnz * static_cast<int64_t>(dsize(desc->solve_dtype))));
+  chk(up(L.eid, c.eid.data(), nnz * 4));
+  chk(up(L.sw, c.sw.data(), c.m * 8));
+  chk(up(L.ubase, c.ubase.data(), (n + 1) * 8));
+  chk(up(L.light, P.light.data(), static_cast<int64_t>(P.light.size()) * 4));
+  chk(up(L.wave_lo, P.wave_lo.data(), static_cast<int64_t>(P.wave_lo.size()) * 4));
+  const int64_t nt = static_cast<int64_t>(P.task_row.size());
+  chk(up(L.task_row, P.task_row.data(), nt * 4));
+  chk(up(L.task_mega, P.task_mega.data(), nt * 4));
+  chk(up(L.task_chunk, P.task_chunk.data(), nt * 4));
+  chk(up(L.task_beg, P.task_beg.data(), nt * 8));
+  chk(up(L.task_end, P.task_end.data(), nt * 8));
+  const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
+  chk(up(L.mega_nchunk, P.mega_nchunk.data(), nm * 4));
+  chk(up(L.mega_chunk0, P.mega_chunk0.data(), nm * 4));
+  const int64_t np = static_cast<int64_t>(P.piece_row.size());
+  chk(up(L.piece_row, P.piece_row.data(), np * 4));
+  chk(up(L.piece_beg, P.piece_beg.data(), np * 8));
+  chk(up(L.piece_end, P.piece_end.data(), np * 8));
+  if (e == hipSuccess) e = hipStreamSynchronize(hs);
+  if (e != hipSuccess) return cleanup(fail(ERC_E_DEVICE, std::string("graph upload: ") + hipGetErrorString(e)));
+  DevGraph& g = h->dg;
+  g.n = static_cast<int32_t>(n);
+  g.nnz = nnz;
+  g.m = c.m;
+  g.weighted = weighted ? 1 : 0;
+  g.rowptr = reinterpret_cast<const int64_t*>(base + L.rowptr);
+  g.col = reinterpret_cast<const int32_t*>(base + L.col);
+  g.w = weighted ? base + L.w : nullptr;
+  g.eid = reinterpret_cast<const int32_t*>(base + L.eid);
+  g.sw = reinterpret_cast<const double*>(base + L.sw);
+  g.ubase = reinterpret_cast<const int64_t*>(base + L.ubase);
+  g.grid = s.grid;
+  g.light = reinterpret_cast<const int32_t*>(base + L.light);
+  g.wave_lo = reinterpret_cast<const int32_t*>(base + L.wave_lo);
+  g.ntask = static_cast<int32_t>(nt);
+  g.task_row = reinterpret_cast<const int32_t*>(base + L.task_row);
+  g.task_mega = reinterpret_cast<const int32_t*>(base + L.task_mega);
+  g.task_chunk = reinterpret_cast<const int32_t*>(base + L.task_chunk);
+  g.task_beg = reinterpret_cast<const int64_t*>(base + L.task_beg);
+  g.task_end = reinterpret_cast<const int64_t*>(base + L.task_end);
+  g.nmega = static_cast<int32_t>(nm);
+  g.mega_nchunk = reinterpret_cast<const int32_t*>(base + L.mega_nchunk);
+  g.mega_chunk0 = reinterpret_cast<const int32_t*>(base + L.mega_chunk0);
+  g.nchunk_slots = P.nslot;
+  g.npiece = np;
+  g.piece_row = reinterpret_cast<const int32_t*>(base + L.piece_row);
+  g.piece_beg = reinterpret_cast<const int64_t*>(base + L.piece_beg);
+  g.piece_end = reinterpret_cast<const int64_t*>(base + L.piece_end);
+  *out = h;
+  return ERC_OK;
+}
+
+erc_status erc_num_nodes(erc_handle h, int64_t* n) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (n == nullptr) return fail(ERC_E_INVALID_ARG, "n is NULL");
+  *n = h->n;
+  return ERC_OK;
+}
+
+erc_status erc_num_edges(erc_handle h, int64_t* m) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (m == nullptr) return fail(ERC_E_INVALID_ARG, "m is NULL");
+  *m = h->m;
+  return ERC_OK;
+}
+
+erc_status erc_edge_endpoints(erc_handle h, int32_t* u_dev, int32_t* v_dev, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (h->m > 0 && (u_dev == nullptr || v_dev == nullptr)) return fail(ERC_E_INVALID_ARG, "output is NULL");
+  ERC_HIP(launch_endpoints(h->dg, u_dev, v_dev, static_cast<hipStream_t>(stream)));
+  return ERC_OK;
+}
+
+erc_status erc_destroy(erc_handle h) {
+  g_last_error.clear();
+  if (h == nullptr) return ERC_OK;
+  if (h->pinned) hipHostFree(h->pinned);
+  for (auto& ev : h->ev)
+    if (ev) hipEventDestroy(ev);
+  for (auto& ev : h->prof)
+    if (ev) hipEventDestroy(ev);
+  delete h;
+  return ERC_OK;
+}
+
+erc_status erc_workspace_bytes(erc_handle h, int32_t k_block, size_t* bytes) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+  if (k_block < 1 || k_block > max_width(h->dt))
+    return fail(ERC_E_INVALID_ARG, "k_block out of range for the working precision");
+  *bytes = static_cast<size_t>(work_layout(h, padded_width(h->dt, k_block)).total);
+  return ERC_OK;
+}
+
+erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws_dev, size_t ws_bytes,
+                          double* R_dev, erc_solve_info* info, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  erc_status st = check_params(h, params);
+  if (st != ERC_OK) return st;
+  if (h->m > 0 && R_dev == nullptr) return fail(ERC_E_INVALID_ARG, "R_dev is NULL");
+  if (ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "ws_dev is NULL");
+  const int kb = padded_width(h->dt, params->k_block);
+  const WorkLayout L = work_layout(h, kb);
+  if (static_cast<int64_t>(ws_bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "workspace smaller than erc_workspace_bytes");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Work w = carve_work(h, kb, ws_dev, L);
+  st = prepare_work(h, w, L, s);
+  if (st != ERC_OK) return st;
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  ERC_HIP(hipEventCreate(&t0));
+  ERC_HIP(hipEventCreate(&t1));
+  ERC_HIP(hipEventRecord(t0, s));
+  BlockStats bs;
+  int blocks = 0;
+  for (int c0 = params->col_begin; c0 < params->col_end; c0 += params->k_block) {
+    const int nc = std::min(params->k_block, params->col_end - c0);
+    const int acc = (c0 == params->col_begin && !(params->flags & ERC_ACCUMULATE)) ? 0 : 1;
+    st = solve_block(h, params, w, c0, nc, h->m > 0 ? R_dev : nullptr, acc, nullptr, &bs, s);
+    if (st != ERC_OK) {
+      hipEventDestroy(t0);
+      hipEventDestroy(t1);
+      return st;
+    }
+    ++blocks;
+  }
+  int64_t bad = 0;
+  if (h->m > 0) {
+    ERC_HIP(launch_count_bad(R_dev, h->m, w, s));
+    double hb = 0.0;
+    ERC_HIP(hipMemcpyAsync(reinterpret_cast<double*>(h->pinned + 2), w.out, 8, hipMemcpyDeviceToHost, s));
+    ERC_HIP(hipEventRecord(t1, s));
+    ERC_HIP(hipStreamSynchronize(s));
+    std::memcpy(&hb, h->pinned + 2, 8);
+    bad = static_cast<int64_t>(hb);
+  } else {
+    ERC_HIP(hipEventRecord(t1, s));
+    ERC_HIP(hipStreamSynchronize(s));
+  }
+  float total = 0.0f;
+  hipEventElapsedTime(&total, t0, t1);
+  hipEventDestroy(t0);
+  hipEventDestroy(t1);
+  if (info) {
+    info->blocks = blocks;
+    info->iters_max = bs.iters_max;
+    info->cols_unconverged = bs.unconverged;
+    info->breakdowns = bs.breakdowns;
+    info->iters_total = bs.iters_total;
+    info->launches = bs.launches;
+    info->nonpositive = bad;
+    info->max_final_relres = bs.max_relres;
+    info->ms_rhs = bs.ms_rhs;
+    info->ms_cg = bs.ms_cg;
+    info->ms_accum = bs.ms_accum;
+    info->ms_total = total;
+    info->ms_spmm = bs.ms_spmm;
+    info->spmm_timed = bs.spmm_timed;
+  }
+  if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown in " + std::to_string(bs.breakdowns) + " column(s)");
+  if (bad > 0) return fail(ERC_E_NUMERIC, std::to_string(bad) + " resistance(s) <= 0 or not finite");
+  if (bs.unconverged > 0)
+    return fail(ERC_E_NOT_CONVERGED, std::to_string(bs.unconverged) + " column(s) reached max_iter");
+  return ERC_OK;
+}
+
+erc_status erc_curvature(erc_handle h, const double* R_dev, double* p_dev, double* kappa_dev,
+                         void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (p_dev == nullptr || (h->m > 0 && (R_dev == nullptr || kappa_dev == nullptr)))
+    return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ERC_HIP(launch_node_p(h->dg, h->dt, R_dev, p_dev, s));
+  ERC_HIP(launch_edge_kappa(h->dg, R_dev, p_dev, kappa_dev, s));
+  return ERC_OK;
+}
+
+namespace {
+struct SampleLayout {
+  int64_t lvl0, lvl1, lvl2, tick, totals, total;
+  int grid;
+};
+SampleLayout sample_layout(const erc_graph_s* h) {
+  SampleLayout L{};
+  const int64_t items = std::max(h->n, h->m);
+  L.grid = static_cast<int>(std::min<int64_t>(kSampleGrid, std::max<int64_t>(1, ceil_div(items, kBlock * 8))));
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off = align_up(off + std::max<int64_t>(bytes, 0), 256);
+    return at;
+  };
+  L.lvl0 = take(static_cast<int64_t>(L.grid) * 3 * 8);
+  L.lvl1 = take(ceil_div(L.grid, kTreeFan) * 3 * 8);
+  L.lvl2 = take(ceil_div(L.grid, kTreeFan * kTreeFan) * 3 * 8);
+  L.tick = take(tree_ticks(L.grid) * 4);
+  L.totals = take(8 * 8);
+  L.total = off;
+  return L;
+}
+}  // namespace
+
+erc_status erc_sampling_scratch_bytes(erc_handle h, size_t* bytes) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+  *bytes = static_cast<size_t>(sample_layout(h).total);
+  return ERC_OK;
+}
+
+erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta, void* scratch_dev,
+                              size_t scratch_bytes, double* node_prob_dev, double* edge_prob_dev,
+                              void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (!(eta > 0.0) || !std::isfinite(eta)) return fail(ERC_E_INVALID_ARG, "eta must be finite and > 0");
+  if (node_prob_dev == nullptr || scratch_dev == nullptr ||
+      (h->m > 0 && (kappa_dev == nullptr || edge_prob_dev == nullptr)))
+    return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const SampleLayout L = sample_layout(h);
+  if (static_cast<int64_t>(scratch_bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_sampling_scratch_bytes");
+  char* b = static_cast<char*>(scratch_dev);
+  SampleWork sw{};
+  sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
+  sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
+  sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
+  sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
+  sw.totals = reinterpret_cast<double*>(b + L.totals);
+  sw.grid = L.grid;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
+  ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
+  ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
+  return ERC_OK;
+}
+
+erc_status erc_debug_check_plan(const erc_graph_desc* desc) {
+  g_last_error.clear();
+  Canon c;
+  erc_status st = canonicalise(desc, &c);
+  if (st != ERC_OK) return st;
+  const int64_t n = desc->n;
+  const int64_t* rp = desc->rowptr;
+  const int64_t nnz = rp[n];
+  const Shape s = make_shape(n, nnz);
+  Plan P;
+  build_plan(desc, c, s, &P);
+  auto bad = [&](const std::string& what) { return fail(ERC_E_STATE, "plan check: " + what); };
+  const int64_t nt = static_cast<int64_t>(P.task_row.size());
+  const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
+  const int64_t np = static_cast<int64_t>(P.piece_row.size());
+  if (nt > s.ntask_max || nm > s.nmega_max || np > s.npiece_max || P.nslot > s.nslot_max)
+    return bad("list exceeds its size bound");
+  if (s.grid < 1 || s.grid > kMaxSpmmGrid || s.waves != s.grid * kWavesPerBlock)
+    return bad("grid shape");
+  // SpMM coverage: each entry once, by a light row or by a block task
+  std::vector<unsigned char> cover(nnz, 0);
+  const int64_t nl = static_cast<int64_t>(P.light.size());
+  if (static_cast<int64_t>(P.wave_lo.size()) != s.waves + 1 || P.wave_lo[0] != 0 ||
+      P.wave_lo[s.waves] != nl)
+    return bad("wave ranges do not span the light rows");
+  for (int w = 0; w < s.waves; ++w)
+    if (P.wave_lo[w] > P.wave_lo[w + 1]) return bad("wave ranges not monotone");
+  std::vector<unsigned char> is_light(n, 0);
+  for (int64_t k = 0; k < nl; ++k) {
+    const int64_t i = P.light[k];
+    if (i < 0 || i >= n || (k > 0 && P.light[k - 1] >= i)) return bad("light rows not ascending in range");
+    if (rp[i + 1] - rp[i] > s.heavy) return bad("light row above the heavy threshold");
+    is_light[i] = 1;
+    for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) cover[pos] += 1;
+  }
+  std::vector<int32_t> seen_chunks(nm, 0);
+  for (int64_t t = 0; t < nt; ++t) {
+    const int64_t i = P.task_row[t];
+    if (i < 0 || i >= n || is_light[i]) return bad("task row out of range or also light");
+    if (P.task_beg[t] < rp[i] || P.task_end[t] > rp[i + 1] || P.task_beg[t] >= P.task_end[t])
+      return bad("task range outside its row");
+    const int32_t mh = P.task_mega[t];
+    if (mh >= 0) {
+      if (mh >= nm || P.task_chunk[t] < 0 || P.task_chunk[t] >= P.mega_nchunk[mh])
+        return bad("chunk index out of range");
+      if (P.mega_chunk0[mh] + P.mega_nchunk[mh] > P.nslot) return bad("chunk slots out of range");
+      seen_chunks[mh] += 1;
+    } else if (P.task_beg[t] != rp[i] || P.task_end[t] != rp[i + 1]) {
+      return bad("single-chunk task does not cover its row");
+    }
+    for (int64_t pos = P.task_beg[t]; pos < P.task_end[t]; ++pos) cover[pos] += 1;
+  }
+  for (int64_t mh = 0; mh < nm; ++mh)
+    if (seen_chunks[mh] != P.mega_nchunk[mh]) return bad("multi-chunk row missing chunks");
+  for (int64_t i = 0; i < n; ++i)
+    if (!is_light[i] && rp[i + 1] - rp[i] <= s.heavy) return bad("row in no plan list");
+  for (int64_t pos = 0; pos < nnz; ++pos)
+    if (cover[pos] != 1) return bad("entry not covered exactly once");
+  // edge pieces: each upper entry once, edge ids consistent with eid
+  std::fill(cover.begin(), cover.end(), 0);
+  for (int64_t t = 0; t < np; ++t) {
+    const int64_t u = P.piece_row[t];
+    if (u < 0 || u >= n) return bad("piece row out of range");
+    const int64_t up = c.ubase[u + 1] - c.ubase[u];
+    const int64_t upos = rp[u + 1] - up;
+    if (P.piece_beg[t] < upos || P.piece_end[t] > rp[u + 1] || P.piece_beg[t] >= P.piece_end[t])
+      return bad("piece outside the upper entries of its row");
+    for (int64_t pos = P.piece_beg[t]; pos < P.piece_end[t]; ++pos) {
+      if (desc->col[pos] <= u) return bad("piece covers a lower entry");
+      const int64_t e = c.ubase[u] + (pos - upos);
+      if (e != c.eid[pos]) return bad("piece edge id differs from the entry's edge id");
+      cover[pos] += 1;
+    }
+  }
+  for (int64_t u = 0; u < n; ++u)
+    for (int64_t pos = rp[u]; pos < rp[u + 1]; ++pos)
+      if ((desc->col[pos] > u) != (cover[pos] == 1)) return bad("upper entry not covered exactly once");
+  return ERC_OK;
+}
+
+erc_status erc_debug_edge_ids(erc_handle h, int32_t* eid_dev, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (h->nnz > 0 && eid_dev == nullptr) return fail(ERC_E_INVALID_ARG, "eid_dev is NULL");
+  ERC_HIP(launch_eids(h->dg, eid_dev, static_cast<hipStream_t>(stream)));
+  return ERC_OK;
+}
+
+erc_status erc_debug_rhs(erc_handle h, int32_t K_total, int32_t col0, int32_t ncols, uint64_t seed,
+                         void* Y_dev, void* ws_dev, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (K_total < 1 || ncols < 1 || ncols > max_width(h->dt) || col0 < 0 || col0 + ncols > K_total)
+    return fail(ERC_E_INVALID_ARG, "bad column range");
+  if (Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const int kb = padded_width(h->dt, ncols);
+  const WorkLayout L = work_layout(h, kb);
+  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Work w = carve_work(h, kb, ws_dev, L);
+  erc_status st = prepare_work(h, w, L, s);
+  if (st != ERC_OK) return st;
+  ERC_HIP(launch_rhs(h->dg, w, h->dt, K_total, col0, ncols, splitmix_first(seed),
+                     1.0 / std::sqrt(static_cast<double>(K_total)), 0.5, s));
+  ERC_HIP(launch_copy_cols(h->dg, w.r, kb, h->dt, ncols, Y_dev, s));
+  return ERC_OK;
+}
+
+erc_status erc_debug_spmm(erc_handle h, double delta, int32_t ncols, const void* X_dev, void* Y_dev,
+                          void* ws_dev, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (ncols < 1 || ncols > max_width(h->dt) || padded_width(h->dt, ncols) != ncols)
+    return fail(ERC_E_INVALID_ARG, "ncols must be a padded block width");
+  if (!std::isfinite(delta) || delta < 0.0) return fail(ERC_E_INVALID_ARG, "delta must be finite and >= 0");
+  if (X_dev == nullptr || Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const WorkLayout L = work_layout(h, ncols);
+  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Work w = carve_work(h, ncols, ws_dev, L);
+  erc_status st = prepare_work(h, w, L, s);
+  if (st != ERC_OK) return st;
+  ERC_HIP(launch_spmm(h->dg, w, h->dt, delta, X_dev, X_dev, Y_dev, w.cs.one, s));
+  return ERC_OK;
+}
+
+erc_status erc_debug_solve_block(erc_handle h, const erc_solve_params* params, int32_t col0,
+                                 int32_t ncols, void* ws_dev, size_t ws_bytes, void* Z_dev,
+                                 int32_t* iters_host, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  erc_status st = check_params(h, params);
+  if (st != ERC_OK) return st;
+  if (ncols < 1 || ncols > params->k_block || col0 < 0 || col0 + ncols > params->K_total)
+    return fail(ERC_E_INVALID_ARG, "bad column range");
+  if (Z_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const int kb = padded_width(h->dt, params->k_block);
+  const WorkLayout L = work_layout(h, kb);
+  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Work w = carve_work(h, kb, ws_dev, L);
+  st = prepare_work(h, w, L, s);
+  if (st != ERC_OK) return st;
+  BlockStats bs;
+  st = solve_block(h, params, w, col0, ncols, nullptr, 0, iters_host, &bs, s);
+  if (st != ERC_OK) return st;
+  ERC_HIP(launch_copy_cols(h->dg, w.z, kb, h->dt, ncols, Z_dev, s));
+  ERC_HIP(hipStreamSynchronize(s));
+  if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown");
+  if (bs.unconverged > 0) return fail(ERC_E_NOT_CONVERGED, "column(s) reached max_iter");
+  return ERC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,1207 @@
+// HIP kernels for gfx950 (CDNA4, wave64) of the resistance-curvature path.
+//
+//   k_rhs        Y = B^T W^{1/2} Q for one column block (Section 3.1.2; Algorithm 1,
+//                forming Y^(t)); also initialises the CG state z = 0, r = p = Y.
+//   k_spmm       q = (L + delta I) p, with the fused dot products p.q, r.q, q.q
+//                (Eq. 5; the matrix-free operator of Section 3.1.3).
+//   k_update     z += alpha p, r -= alpha q, p = r + beta p, and r.r (column-wise CG,
+//                Section 3.1.3; Algorithm 1).
+//   k_edge_dist  R_e += sum_c (z_uc - z_vc)^2 (Eq. 6; Algorithm 1, edge blocks).
+//   k_node_p, k_edge_kappa   node and edge curvature (Eq. 2).
+//   k_minmax, k_node_w, k_edge_w, k_normalise   sampling probabilities (Eqs. 7, 8).
+//
+// Layout: every n x kb block (z, r, p, q) is row-major with kb a power of two, so one
+// row is 64..1024 bytes.  In the gather kernels a row is read by LPN lanes with one
+// 16-byte load each and a wavefront covers NPW = 64 / LPN neighbours per instruction.
+//
+// Determinism: no floating-point atomics anywhere.  Each block reduces its partial
+// sums in a fixed order and the grid combines block partials through a fixed-fan-in
+// tree (tree_sum): an integer ticket only elects which block performs each level, the
+// summation order is a function of the grid size alone.  Results are therefore
+// bit-identical from run to run.
+#include <hip/hip_runtime.h>
+
+#include "erc_common.h"
+
+namespace erc {
+namespace {
+
+template <typename T>
+struct __attribute__((aligned(16))) V {
+  static constexpr int N = 16 / sizeof(T);
+  T x[N];
+};
+
+template <typename T>
+__device__ __forceinline__ V<T> ldv(const T* p) {
+  return *reinterpret_cast<const V<T>*>(p);
+}
+template <typename T>
+__device__ __forceinline__ void stv(T* p, const V<T>& v) {
+  *reinterpret_cast<V<T>*>(p) = v;
+}
+template <typename T>
+__device__ __forceinline__ V<T> vzero() {
+  V<T> v;
+#pragma unroll
+  for (int k = 0; k < V<T>::N; ++k) v.x[k] = T(0);
+  return v;
+}
+
+__device__ __forceinline__ double readlane_f64(double x, int k) {
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane(static_cast<int>(b & 0xffffffffll), k);
+  const int hi = __builtin_amdgcn_readlane(static_cast<int>(b >> 32), k);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) |
+                              (static_cast<unsigned int>(lo)));
+}
+
+// SplitMix64 output finaliser (Steele, Lea & Flood 2014).
+__device__ __forceinline__ uint64_t splitmix_final(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+// Output number `ctr` of SplitMix64 started from state `base`.
+__device__ __forceinline__ uint64_t splitmix_at(uint64_t base, uint64_t ctr) {
+  return splitmix_final(base + (ctr + 1ull) * 0x9E3779B97F4A7C15ull);
+}
+
+// ---------------------------------------------------------------------------------
+// Inner products are accumulated in at least twice the working precision: fp32
+// products are exact in fp64 and are summed in fp64; fp64 products are split exactly
+// (fma) and summed as double-double pairs (Knuth's TwoSum), so the CG coefficients do
+// not inherit the summation error of a plain fp64 sum.
+struct DDv {
+  double s, c;  // value s + c
+};
+
+__device__ __forceinline__ void two_sum_d(double a, double b, double& s, double& e) {
+#pragma clang fp contract(off)
+  s = a + b;
+  const double z = s - a;
+  e = (a - (s - z)) + (b - z);
+}
+
+__device__ __forceinline__ DDv dd_add(const DDv& a, const DDv& b) {
+#pragma clang fp contract(off)
+  double s, e;
+  two_sum_d(a.s, b.s, s, e);
+  DDv r;
+  r.s = s;
+  r.c = (a.c + b.c) + e;
+  return r;
+}
+
+__device__ __forceinline__ DDv dd_mul_d(const DDv& a, double b) {
+#pragma clang fp contract(off)
+  const double p = a.s * b;
+  const double pe = fma(a.s, b, -p);
+  const double c = pe + a.c * b;
+  DDv r;
+  two_sum_d(p, c, r.s, r.c);
+  return r;
+}
+
+__device__ __forceinline__ double dd_value(const DDv& a) { return a.s + a.c; }
+
+template <typename T>
+struct Dot;
+template <>
+struct Dot<float> {
+  double s = 0.0;
+  __device__ __forceinline__ void add(float x, float y) {
+    s = fma(static_cast<double>(x), static_cast<double>(y), s);  // exact product, one rounding
+  }
+  __device__ __forceinline__ DDv get() const { return DDv{s, 0.0}; }
+  __device__ __forceinline__ static DDv one(float x, float y) {
+    return DDv{static_cast<double>(x) * static_cast<double>(y), 0.0};
+  }
+};
+template <>
+struct Dot<double> {
+  double s = 0.0, c = 0.0;
+  __device__ __forceinline__ void add(double x, double y) {
+#pragma clang fp contract(off)
+    const double p = x * y;
+    const double pe = fma(x, y, -p);
+    double t, e;
+    two_sum_d(s, p, t, e);
+    s = t;
+    c += e + pe;
+  }
+  __device__ __forceinline__ DDv get() const { return DDv{s, c}; }
+  __device__ __forceinline__ static DDv one(double x, double y) {
+#pragma clang fp contract(off)
+    const double p = x * y;
+    return DDv{p, fma(x, y, -p)};
+  }
+};
+
+// ---------------------------------------------------------------------------------
+// Deterministic grid reduction.  `in` (LDS, nval doubles) holds this block's values.
+// Returns true in exactly one block, with the grid totals in `out` (LDS).  All threads
+// of every block must call it.  Tickets are left at zero for the next launch.
+template <class Op>
+__device__ bool tree_reduce(const Tree& t, int nval, const double* in, double* out) {
+  __shared__ int s_last;
+  const int tid = threadIdx.x;
+  if (gridDim.x == 1) {
+    for (int v = tid; v < nval; v += blockDim.x) out[v] = in[v];
+    __syncthreads();
+    return true;
+  }
+  for (int v = tid; v < nval; v += blockDim.x)
+    t.lvl0[static_cast<size_t>(blockIdx.x) * nval + v] = in[v];
+  int cnt = gridDim.x;
+  int idx = blockIdx.x;
+  const double* src = t.lvl0;
+  uint32_t* tick = t.tick;
+  for (int level = 0;; ++level) {
+    const int ng = (cnt + kTreeFan - 1) / kTreeFan;
+    const int grp = idx / kTreeFan;
+    const int gsize = min(kTreeFan, cnt - grp * kTreeFan);
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) s_last = (atomicAdd(&tick[grp], 1u) == static_cast<unsigned>(gsize - 1));
+    __syncthreads();
+    if (!s_last) return false;
+    __threadfence();
+    double* dst = (ng == 1) ? out : (level == 0 ? t.lvl1 : t.lvl2) + static_cast<size_t>(grp) * nval;
+    for (int v = tid; v < nval; v += blockDim.x) {
+      const double* b = src + static_cast<size_t>(grp) * kTreeFan * nval + v;
+      double s = b[0];
+      for (int k = 1; k < gsize; ++k) s = Op::apply(s, b[static_cast<size_t>(k) * nval]);
+      dst[v] = s;
+    }
+    if (tid == 0) tick[grp] = 0u;
+    if (ng == 1) {
+      __syncthreads();
+      return true;
+    }
+    src = (level == 0) ? t.lvl1 : t.lvl2;
+    tick += ng;
+    cnt = ng;
+    idx = grp;
+  }
+}
+struct OpSum {
+  __device__ static double apply(double a, double b) { return a + b; }
+};
+struct OpMax {
+  __device__ static double apply(double a, double b) { return a > b ? a : b; }
+};
+
+// The same tree for compensated pairs: `in`/`out` are LDS arrays of nval pairs and the
+// level buffers hold nval pairs per block.
+__device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
+  __shared__ int s_last;
+  const int tid = threadIdx.x;
+  if (gridDim.x == 1) {
+    for (int v = tid; v < nval; v += blockDim.x) out[v] = in[v];
+    __syncthreads();
+    return true;
+  }
+  DDv* l0 = reinterpret_cast<DDv*>(t.lvl0);
+  for (int v = tid; v < nval; v += blockDim.x) l0[static_cast<size_t>(blockIdx.x) * nval + v] = in[v];
+  int cnt = gridDim.x;
+  int idx = blockIdx.x;
+  const DDv* src = l0;
+  uint32_t* tick = t.tick;
+  for (int level = 0;; ++level) {
+    const int ng = (cnt + kTreeFan - 1) / kTreeFan;
+    const int grp = idx / kTreeFan;
+    const int gsize = min(kTreeFan, cnt - grp * kTreeFan);
+    __threadfence();
+    __syncthreads();
+    if (tid == 0) s_last = (atomicAdd(&tick[grp], 1u) == static_cast<unsigned>(gsize - 1));
+    __syncthreads();
+    if (!s_last) return false;
+    __threadfence();
+    DDv* lvl = reinterpret_cast<DDv*>(level == 0 ? t.lvl1 : t.lvl2);
+    DDv* dst = (ng == 1) ? out : lvl + static_cast<size_t>(grp) * nval;
+    for (int v = tid; v < nval; v += blockDim.x) {
+      const DDv* b = src + static_cast<size_t>(grp) * kTreeFan * nval + v;
+      DDv acc = b[0];
+      for (int k = 1; k < gsize; ++k) acc = dd_add(acc, b[static_cast<size_t>(k) * nval]);
+      dst[v] = acc;
+    }
+    if (tid == 0) tick[grp] = 0u;
+    if (ng == 1) {
+      __syncthreads();
+      return true;
+    }
+    src = lvl;
+    tick += ng;
+    cnt = ng;
+    idx = grp;
+  }
+}
+
+// ---------------------------------------------------------------------------------
+// Neighbour gather of one row range: acc += w_ij (p_i - p_j) over CSR entries
+// [beg, end) of row i.  Lane (grp, sub) handles neighbour slot grp of each step and
+// columns [sub*VEC, sub*VEC + VEC).  Slots past the end read p_i (weight 0), which
+// adds exactly zero, so the loop has no per-load predicate.
+template <typename T, int LPN, bool W>
+__device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
+                                           const T* __restrict__ wgt, const T* __restrict__ P,
+                                           int i, int64_t beg, int64_t end, const V<T>& pi,
+                                           V<T>& acc, int lane) {
+  constexpr int VEC = V<T>::N;
+  constexpr int KB = LPN * VEC;
+  constexpr int NPW = 64 / LPN;
+  const int grp = lane / LPN;
+  const int sub = lane % LPN;
+  for (int64_t base = beg; base < end; base += 64) {
+    const int cnt = static_cast<int>(min(static_cast<int64_t>(64), end - base));
+    int myj = i;
+    T myw = T(0);
+    if (lane < cnt) {
+      myj = __builtin_nontemporal_load(col + base + lane);
+      if (W) myw = __builtin_nontemporal_load(wgt + base + lane);
+    }
+    const int steps = (cnt + NPW - 1) / NPW;
+#pragma unroll 4
+    for (int st = 0; st < steps; ++st) {
+      const int k = st * NPW + grp;
+      const int j = __shfl(myj, k);
+      const V<T> pj = ldv(P + static_cast<int64_t>(j) * KB + sub * VEC);
+      if (W) {
+        const T wj = __shfl(myw, k);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc.x[v] += wj * (pi.x[v] - pj.x[v]);
+      } else {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc.x[v] += pi.x[v] - pj.x[v];
+      }
+    }
+  }
+}
+
+// Sum acc over the NPW neighbour groups of the wavefront (xor butterfly: every lane
+// ends with the same, order-fixed total).
+template <typename T, int LPN>
+__device__ __forceinline__ void reduce_groups(V<T>& acc) {
+#pragma unroll
+  for (int off = LPN; off < 64; off <<= 1) {
+#pragma unroll
+    for (int v = 0; v < V<T>::N; ++v) acc.x[v] += __shfl_xor(acc.x[v], off);
+  }
+}
+
+struct SpmmArgs {
+  DevGraph g;
+  const void* p;
+  const void* r;
+  void* q;
+  void* chunkbuf;
+  double* mega_dots;  // nmega x 3 x kb pairs
+  uint32_t* mega_tick;
+  Tree tree;
+  ColState cs;
+  const int32_t* gate;
+  double delta;
+  int finalise;  // 1: compute alpha, beta from the dot products
+};
+
+// q = (L + delta I) p for a block of kb = LPN*VEC columns, plus per-column p.q, r.q,
+// q.q accumulated in at least twice the working precision.  Block tasks (long rows,
+// split over the 4 waves of a block and, beyond one block's share, over several
+// blocks) run first; then each wave walks its own contiguous range of short rows.
+template <typename T, int LPN, bool W>
+__global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
+  constexpr int VEC = V<T>::N;
+  constexpr int KB = LPN * VEC;
+  if (*a.gate == 0) return;
+  __shared__ DDv s_dots[kWavesPerBlock][3 * KB];
+  __shared__ V<T> s_acc[kWavesPerBlock][LPN];
+  __shared__ int s_last;
+
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int sub = lane % LPN;
+  const T* __restrict__ P = static_cast<const T*>(a.p);
+  const T* __restrict__ Rr = static_cast<const T*>(a.r);
+  T* __restrict__ Q = static_cast<T*>(a.q);
+  const T* __restrict__ wgt = static_cast<const T*>(a.g.w);
+  const T dlt = static_cast<T>(a.delta);
+
+  Dot<T> dpq[VEC], drq[VEC], dqq[VEC];
+
+  // finish one row in group-0 lanes: q = delta p_i + acc, store, accumulate the dots
+  // (into this lane's partials, or as this row's own pairs at `dst`)
+  auto finish = [&](int i, const V<T>& pi, const V<T>& acc, DDv* dst) {
+    V<T> qv;
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
+    const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
+    stv(Q + off, qv);
+    const V<T> ri = ldv(Rr + off);
+    if (dst == nullptr) {
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) {
+        dpq[v].add(pi.x[v], qv.x[v]);
+        drq[v].add(ri.x[v], qv.x[v]);
+        dqq[v].add(qv.x[v], qv.x[v]);
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) {
+        dst[sub * VEC + v] = Dot<T>::one(pi.x[v], qv.x[v]);
+        dst[KB + sub * VEC + v] = Dot<T>::one(ri.x[v], qv.x[v]);
+        dst[2 * KB + sub * VEC + v] = Dot<T>::one(qv.x[v], qv.x[v]);
+      }
+    }
+  };
+
+  // 1. block-cooperative tasks
+  for (int t = blockIdx.x; t < a.g.ntask; t += gridDim.x) {
+    const int i = a.g.task_row[t];
+    const int64_t tb = a.g.task_beg[t];
+    const int64_t len = a.g.task_end[t] - tb;
+    const int64_t wb = tb + (len * wv) / kWavesPerBlock;
+    const int64_t we = tb + (len * (wv + 1)) / kWavesPerBlock;
+    const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
+    V<T> acc = vzero<T>();
+    gather_row<T, LPN, W>(a.g.col, wgt, P, i, wb, we, pi, acc, lane);
+    reduce_groups<T, LPN>(acc);
+    if (lane < LPN) s_acc[wv][sub] = acc;
+    __syncthreads();
+    const int mh = a.g.task_mega[t];
+    V<T> tot = vzero<T>();
+    if (wv == 0 && lane < LPN) {
+#pragma unroll
+      for (int w = 0; w < kWavesPerBlock; ++w) {
+        const V<T> x = s_acc[w][sub];
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) tot.x[v] += x.x[v];
+      }
+    }
+    if (mh < 0) {
+      if (wv == 0 && lane < LPN) finish(i, pi, tot, nullptr);
+    } else {
+      T* cb = static_cast<T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
+      if (wv == 0 && lane < LPN) stv(cb + static_cast<int64_t>(a.g.task_chunk[t]) * KB + sub * VEC, tot);
+      __threadfence();
+      __syncthreads();
+      if (threadIdx.x == 0)
+        s_last = (atomicAdd(&a.mega_tick[mh], 1u) ==
+                  static_cast<unsigned>(a.g.mega_nchunk[mh] - 1));
+      __syncthreads();
+      if (s_last) {
+        __threadfence();
+        if (wv == 0 && lane < LPN) {
+          V<T> rs = vzero<T>();
+          const int nch = a.g.mega_nchunk[mh];
+          for (int k = 0; k < nch; ++k) {
+            const V<T> x = ldv(cb + static_cast<int64_t>(k) * KB + sub * VEC);
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) rs.x[v] += x.x[v];
+          }
+          finish(i, pi, rs, reinterpret_cast<DDv*>(a.mega_dots) + static_cast<int64_t>(mh) * 3 * KB);
+        }
+        if (threadIdx.x == 0) a.mega_tick[mh] = 0u;
+      }
+    }
+    __syncthreads();
+  }
+
+  // 2. this wave's short rows
+  {
+    const int gw = blockIdx.x * kWavesPerBlock + wv;
+    const int lo = a.g.wave_lo[gw];
+    const int hi = a.g.wave_lo[gw + 1];
+    for (int k = lo; k < hi; ++k) {
+      const int i = a.g.light[k];
+      const int64_t b = a.g.rowptr[i];
+      const int64_t e = a.g.rowptr[i + 1];
+      const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
+      V<T> acc = vzero<T>();
+      gather_row<T, LPN, W>(a.g.col, wgt, P, i, b, e, pi, acc, lane);
+      reduce_groups<T, LPN>(acc);
+      if (lane < LPN) finish(i, pi, acc, nullptr);
+    }
+  }
+
+  // 3. block partials of the three dot products (waves in order), then the grid tree
+  if (lane < LPN) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+      s_dots[wv][sub * VEC + v] = dpq[v].get();
+      s_dots[wv][KB + sub * VEC + v] = drq[v].get();
+      s_dots[wv][2 * KB + sub * VEC + v] = dqq[v].get();
+    }
+  }
+  __syncthreads();
+  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
+    DDv acc = s_dots[0][v];
+#pragma unroll
+    for (int w = 1; w < kWavesPerBlock; ++w) acc = dd_add(acc, s_dots[w][v]);
+    s_dots[0][v] = acc;
+  }
+  __syncthreads();
+  DDv* s_out = s_dots[1];
+  if (!tree_sum_dd(a.tree, 3 * KB, s_dots[0], s_out)) return;
+  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
+  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
+    DDv acc = s_out[v];
+    for (int mh = 0; mh < a.g.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
+    s_out[v] = acc;
+  }
+  __syncthreads();
+  if (!a.finalise) return;
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    if (a.cs.active[c]) {
+      const double pq = dd_value(s_out[c]);
+      const DDv rq = s_out[KB + c];
+      const DDv qq = s_out[2 * KB + c];
+      const double rho = a.cs.rho[c];
+      if (!(pq > 0.0) || !isfinite(pq) || !isfinite(dd_value(rq)) || !isfinite(dd_value(qq))) {
+        a.cs.active[c] = 0;
+        a.cs.status[c] = 1;
+        a.cs.alpha[c] = 0.0;
+        a.cs.beta[c] = 0.0;
+      } else {
+        // rho' = ||r - alpha q||^2 = rho - 2 alpha r.q + alpha^2 q.q, evaluated in
+        // double-double; the exact r.r is recomputed by k_update and used for the
+        // stopping test and the next alpha.
+        const double al = rho / pq;
+        const DDv t1 = dd_mul_d(rq, -2.0 * al);
+        const DDv t2 = dd_mul_d(dd_mul_d(qq, al), al);
+        const double rf = dd_value(dd_add(dd_add(DDv{rho, 0.0}, t1), t2));
+        a.cs.alpha[c] = al;
+        a.cs.beta[c] = (rf > 0.0 ? rf : 0.0) / rho;
+      }
+    } else {
+      a.cs.alpha[c] = 0.0;
+      a.cs.beta[c] = 0.0;
+    }
+  }
+}
+
+struct UpdArgs {
+  void* z;
+  void* r;
+  void* p;
+  const void* q;
+  int64_t nvec;  // n * kb / VEC
+  Tree tree;
+  ColState cs;
+};
+
+// z += alpha p; r -= alpha q; p = r + beta p (active columns); rho' = r.r in at least
+// twice the working precision.  Thread x of the grid-stride loop always covers column
+// group x % CG, so each thread keeps fixed-column partials.
+template <typename T, int CG>
+__global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
+  constexpr int VEC = V<T>::N;
+  constexpr int KB = CG * VEC;
+  static_assert(kBlock % CG == 0, "column groups must divide the block");
+  if (*a.cs.n_active == 0) return;
+  __shared__ DDv s_part[kBlock][VEC];
+  __shared__ DDv s_in[KB];
+  __shared__ DDv s_out[KB];
+  const int cg = threadIdx.x % CG;
+  T al[VEC], be[VEC];
+  bool act[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) {
+    const int c = cg * VEC + v;
+    al[v] = static_cast<T>(a.cs.alpha[c]);
+    be[v] = static_cast<T>(a.cs.beta[c]);
+    act[v] = a.cs.active[c] != 0;
+  }
+  Dot<T> part[VEC];
+  T* __restrict__ Z = static_cast<T*>(a.z);
+  T* __restrict__ R = static_cast<T*>(a.r);
+  T* __restrict__ P = static_cast<T*>(a.p);
+  const T* __restrict__ Qv = static_cast<const T*>(a.q);
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < a.nvec; x += stride) {
+    const int64_t o = x * VEC;
+    V<T> z = ldv(Z + o), r = ldv(R + o), p = ldv(P + o);
+    const V<T> q = ldv(Qv + o);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+      z.x[v] += al[v] * p.x[v];
+      r.x[v] -= al[v] * q.x[v];
+      if (act[v]) p.x[v] = r.x[v] + be[v] * p.x[v];
+      part[v].add(r.x[v], r.x[v]);
+    }
+    stv(Z + o, z);
+    stv(R + o, r);
+    stv(P + o, p);
+  }
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) s_part[threadIdx.x][v] = part[v].get();
+  __syncthreads();
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    const int g = c / VEC, v = c % VEC;
+    DDv acc = s_part[g][v];
+    for (int t = g + CG; t < kBlock; t += CG) acc = dd_add(acc, s_part[t][v]);
+    s_in[c] = acc;
+  }
+  __syncthreads();
+  if (!tree_sum_dd(a.tree, KB, s_in, s_out)) return;
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    if (a.cs.active[c]) {
+      const double rn = dd_value(s_out[c]);
+      a.cs.iters[c] += 1;
+      a.cs.rho[c] = rn;
+      if (!(rn > a.cs.thr[c])) {
+        a.cs.active[c] = 0;
+        if (!isfinite(rn)) a.cs.status[c] = 1;
+      }
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int cnt = 0;
+    for (int c = 0; c < KB; ++c) cnt += a.cs.active[c] != 0;
+    *a.cs.n_active = cnt;
+  }
+}
+
+struct RhsArgs {
+  DevGraph g;
+  void* z;
+  void* r;
+  void* p;
+  int col0;
+  int ncols;
+  uint64_t words;  // 64-bit sign words per edge, ceil(K/64)
+  uint64_t base;   // SplitMix64 state the sign stream starts from
+  double inv_sqrt_k;
+  double tol2;
+  Tree tree;
+  ColState cs;
+};
+
+// One wavefront per row; lane l holds columns l, l+64, ... of the block.  The sum over
+// the row's neighbours runs in ascending CSR order in fp64 and is rounded once, so Y is
+// reproducible bit for bit.  Edge ids, neighbours and sqrt(w) are loaded 64 at a time
+// and read back with readlane, which keeps the sign-word hash wave-uniform.
+template <typename T, int KB>
+__global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
+  constexpr int CPL = (KB + 63) / 64;
+  __shared__ DDv s_part[kWavesPerBlock][KB];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  T* __restrict__ Z = static_cast<T*>(a.z);
+  T* __restrict__ R = static_cast<T*>(a.r);
+  T* __restrict__ Pp = static_cast<T*>(a.p);
+  const bool aligned = (a.col0 & 63) == 0;
+  Dot<T> r0[CPL];
+  const int nw = gridDim.x * kWavesPerBlock;
+  for (int i = blockIdx.x * kWavesPerBlock + wv; i < a.g.n; i += nw) {
+    double acc[CPL];
+#pragma unroll
+    for (int cl = 0; cl < CPL; ++cl) acc[cl] = 0.0;
+    const int64_t b = a.g.rowptr[i];
+    const int64_t e = a.g.rowptr[i + 1];
+    for (int64_t base = b; base < e; base += 64) {
+      const int cnt = static_cast<int>(min(static_cast<int64_t>(64), e - base));
+      int myj = 0, mye = 0;
+      double mysw = 0.0;
+      if (lane < cnt) {
+        myj = a.g.col[base + lane];
+        mye = a.g.eid[base + lane];
+        mysw = a.g.sw[mye];
+      }
+      for (int k = 0; k < cnt; ++k) {
+        const int j = __builtin_amdgcn_readlane(myj, k);
+        const int ee = __builtin_amdgcn_readlane(mye, k);
+        const double s = readlane_f64(mysw, k);
+        const double t = (i < j) ? s : -s;  // B_{e,i}: +1 at the smaller endpoint
+        const uint64_t ctr0 = static_cast<uint64_t>(ee) * a.words;
+#pragma unroll
+        for (int cl = 0; cl < CPL; ++cl) {
+          const int c = a.col0 + cl * 64 + lane;  // global column of this lane
+          const int wlo = (a.col0 + cl * 64) >> 6;
+          uint64_t word = splitmix_at(a.base, ctr0 + wlo);
+          if (!aligned) {
+            const uint64_t whi = splitmix_at(a.base, ctr0 + wlo + 1);
+            word = ((c >> 6) == wlo) ? word : whi;
+          }
+          const bool neg = (word >> (c & 63)) & 1ull;
+          acc[cl] += neg ? -t : t;
+        }
+      }
+    }
+#pragma unroll
+    for (int cl = 0; cl < CPL; ++cl) {
+      const int cc = cl * 64 + lane;
+      if (cc < KB) {
+        const T y = (cc < a.ncols) ? static_cast<T>(acc[cl] * a.inv_sqrt_k) : T(0);
+        const int64_t o = static_cast<int64_t>(i) * KB + cc;
+        R[o] = y;
+        Pp[o] = y;
+        Z[o] = T(0);
+        r0[cl].add(y, y);
+      }
+    }
+  }
+#pragma unroll
+  for (int cl = 0; cl < CPL; ++cl) {
+    const int cc = cl * 64 + lane;
+    if (cc < KB) s_part[wv][cc] = r0[cl].get();
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    DDv acc = s_part[0][c];
+#pragma unroll
+    for (int w = 1; w < kWavesPerBlock; ++w) acc = dd_add(acc, s_part[w][c]);
+    s_part[0][c] = acc;
+  }
+  __syncthreads();
+  DDv* s_out = s_part[1];
+  if (!tree_sum_dd(a.tree, KB, s_part[0], s_out)) return;
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    const double rr = dd_value(s_out[c]);
+    a.cs.rho[c] = rr;
+    a.cs.rho0[c] = rr;
+    a.cs.thr[c] = a.tol2 * rr;
+    a.cs.active[c] = (c < a.ncols && rr > 0.0) ? 1 : 0;
+    a.cs.iters[c] = 0;
+    a.cs.status[c] = 0;
+    a.cs.alpha[c] = 0.0;
+    a.cs.beta[c] = 0.0;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int cnt = 0;
+    for (int c = 0; c < KB; ++c) cnt += a.cs.active[c] != 0;
+    *a.cs.n_active = cnt;
+  }
+}
+
+// R_e (+)= sum_c (z_uc - z_vc)^2 over the upper entries (v > u) of each piece.  The
+// squared difference is formed in fp64; LPN lanes sum one edge's columns.
+template <typename T, int LPN>
+__global__ __launch_bounds__(kBlock) void k_edge_dist(DevGraph g, const T* __restrict__ Z,
+                                                      double* __restrict__ R, int accumulate) {
+  constexpr int VEC = V<T>::N;
+  constexpr int KB = LPN * VEC;
+  constexpr int NPW = 64 / LPN;
+  const int lane = threadIdx.x & 63;
+  const int grp = lane / LPN;
+  const int sub = lane % LPN;
+  const int64_t nw = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+       t < g.npiece; t += nw) {
+    const int u = g.piece_row[t];
+    const int64_t pb = g.piece_beg[t];
+    const int64_t pe = g.piece_end[t];
+    const int64_t upos = g.rowptr[u + 1] - (g.ubase[u + 1] - g.ubase[u]);
+    const int64_t ebase = g.ubase[u] + (pb - upos);
+    const V<T> zu = ldv(Z + static_cast<int64_t>(u) * KB + sub * VEC);
+    for (int64_t base = pb; base < pe; base += 64) {
+      const int cnt = static_cast<int>(min(static_cast<int64_t>(64), pe - base));
+      const int myj = (lane < cnt) ? g.col[base + lane] : u;
+      const int steps = (cnt + NPW - 1) / NPW;
+      for (int st = 0; st < steps; ++st) {
+        const int k = st * NPW + grp;
+        const int j = __shfl(myj, k);
+        const V<T> zv = ldv(Z + static_cast<int64_t>(j) * KB + sub * VEC);
+        double d = 0.0;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+          const double df = static_cast<double>(zu.x[v]) - static_cast<double>(zv.x[v]);
+          d += df * df;
+        }
+#pragma unroll
+        for (int off = 1; off < LPN; off <<= 1) d += __shfl_xor(d, off);
+        if (sub == 0 && k < cnt) {
+          const int64_t ed = ebase + (base - pb) + k;
+          R[ed] = accumulate ? R[ed] + d : d;
+        }
+      }
+    }
+  }
+}
+
+// p_u = 1 - 1/2 sum_v w_uv R_e(u,v): one wavefront per row, lanes striding the row.
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_node_p(DevGraph g, const double* __restrict__ R,
+                                                   double* __restrict__ p) {
+  const int lane = threadIdx.x & 63;
+  const int nw = gridDim.x * kWavesPerBlock;
+  const T* __restrict__ w = static_cast<const T*>(g.w);
+  for (int i = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6); i < g.n; i += nw) {
+    const int64_t b = g.rowptr[i], e = g.rowptr[i + 1];
+    double s = 0.0;
+    for (int64_t pos = b + lane; pos < e; pos += 64) {
+      const double wt = g.weighted ? static_cast<double>(w[pos]) : 1.0;
+      s += wt * R[g.eid[pos]];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) p[i] = 1.0 - 0.5 * s;
+  }
+}
+
+// kappa_e = 2 (p_u + p_v) / R_e over the edge pieces, one lane per edge.
+__global__ __launch_bounds__(kBlock) void k_edge_kappa(DevGraph g, const double* __restrict__ R,
+                                                       const double* __restrict__ p,
+                                                       double* __restrict__ kappa) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+       t < g.npiece; t += nw) {
+    const int u = g.piece_row[t];
+    const int64_t pb = g.piece_beg[t], pe = g.piece_end[t];
+    const int64_t upos = g.rowptr[u + 1] - (g.ubase[u + 1] - g.ubase[u]);
+    const int64_t ebase = g.ubase[u] + (pb - upos);
+    const double pu = p[u];
+    for (int64_t pos = pb + lane; pos < pe; pos += 64) {
+      const int64_t e = ebase + (pos - pb);
+      kappa[e] = 2.0 * (pu + p[g.col[pos]]) / R[e];
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_endpoints(DevGraph g, int32_t* __restrict__ eu,
+                                                      int32_t* __restrict__ ev) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nw = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
+       t < g.npiece; t += nw) {
+    const int u = g.piece_row[t];
+    const int64_t pb = g.piece_beg[t], pe = g.piece_end[t];
+    const int64_t upos = g.rowptr[u + 1] - (g.ubase[u + 1] - g.ubase[u]);
+    const int64_t ebase = g.ubase[u] + (pb - upos);
+    for (int64_t pos = pb + lane; pos < pe; pos += 64) {
+      const int64_t e = ebase + (pos - pb);
+      eu[e] = u;
+      ev[e] = g.col[pos];
+    }
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t* p, uint32_t v, int64_t count) {
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < count;
+       x += static_cast<int64_t>(gridDim.x) * kBlock)
+    p[x] = v;
+}
+__global__ __launch_bounds__(kBlock) void k_fill_f64(double* p, double v, int64_t count) {
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < count;
+       x += static_cast<int64_t>(gridDim.x) * kBlock)
+    p[x] = v;
+}
+
+// count of entries that are <= 0 or not finite -> out[0]
+__global__ __launch_bounds__(kBlock) void k_count_bad(const double* __restrict__ x, int64_t count,
+                                                      Tree tree, double* out) {
+  __shared__ double s_w[kWavesPerBlock];
+  __shared__ double s_in[1], s_out[1];
+  double c = 0.0;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const double v = x[i];
+    c += (!(v > 0.0) || !isfinite(v)) ? 1.0 : 0.0;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = s_w[0];
+    for (int w = 1; w < kWavesPerBlock; ++w) s += s_w[w];
+    s_in[0] = s;
+  }
+  __syncthreads();
+  if (!tree_reduce<OpSum>(tree, 1, s_in, s_out)) return;
+  if (threadIdx.x == 0) out[0] = s_out[0];
+}
+
+// dst (n x ncols, row-major) = the first ncols columns of src (n x kb)
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_copy_cols(const T* __restrict__ src, int kb,
+                                                      T* __restrict__ dst, int ncols, int64_t n) {
+  const int64_t total = n * ncols;
+  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < total;
+       x += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const int64_t i = x / ncols;
+    const int c = static_cast<int>(x - i * ncols);
+    dst[x] = src[i * kb + c];
+  }
+}
+
+// ---- sampling (Eqs. 7, 8) --------------------------------------------------------
+
+// totals[0] = -kappa_min, totals[1] = kappa_max, totals[4] = 1 if any kappa is not finite
+__global__ __launch_bounds__(kBlock) void k_minmax(const double* __restrict__ kappa, int64_t m,
+                                                   Tree tree, double* totals) {
+  __shared__ double s_w[kWavesPerBlock][3];
+  __shared__ double s_in[3], s_out[3];
+  double nmn = -INFINITY, mx = -INFINITY, bad = 0.0;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < m;
+       e += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const double k = kappa[e];
+    if (isfinite(k)) {
+      nmn = fmax(nmn, -k);
+      mx = fmax(mx, k);
+    } else {
+      bad = 1.0;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    nmn = fmax(nmn, __shfl_xor(nmn, off));
+    mx = fmax(mx, __shfl_xor(mx, off));
+    bad = fmax(bad, __shfl_xor(bad, off));
+  }
+  if ((threadIdx.x & 63) == 0) {
+    s_w[threadIdx.x >> 6][0] = nmn;
+    s_w[threadIdx.x >> 6][1] = mx;
+    s_w[threadIdx.x >> 6][2] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    double s = s_w[0][threadIdx.x];
+    for (int w = 1; w < kWavesPerBlock; ++w) s = fmax(s, s_w[w][threadIdx.x]);
+    s_in[threadIdx.x] = s;
+  }
+  __syncthreads();
+  if (!tree_reduce<OpMax>(tree, 3, s_in, s_out)) return;
+  if (threadIdx.x == 0) {
+    totals[0] = s_out[0];
+    totals[1] = s_out[1];
+    totals[4] = s_out[2];
+  }
+}
+
+// q_u = sum_v (kappa_uv - kappa_min) / (kappa_max - kappa_min + eta) -> pn[u]; sum -> totals[2]
+__global__ __launch_bounds__(kBlock) void k_node_w(DevGraph g, const double* __restrict__ kappa,
+                                                   double eta, Tree tree, double* totals,
+                                                   double* __restrict__ pn) {
+  __shared__ double s_w[kWavesPerBlock];
+  __shared__ double s_in[1], s_out[1];
+  const double kmin = -totals[0];
+  const double kmax = totals[1];
+  const double den = kmax - kmin + eta;
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  const int nw = gridDim.x * kWavesPerBlock;
+  double acc = 0.0;
+  for (int i = blockIdx.x * kWavesPerBlock + wv; i < g.n; i += nw) {
+    const int64_t b = g.rowptr[i], e = g.rowptr[i + 1];
+    double s = 0.0;
+    for (int64_t pos = b + lane; pos < e; pos += 64) s += (kappa[g.eid[pos]] - kmin) / den;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if (lane == 0) pn[i] = s;
+    acc += s;  // identical in every lane
+  }
+  if (lane == 0) s_w[wv] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = s_w[0];
+    for (int w = 1; w < kWavesPerBlock; ++w) s += s_w[w];
+    s_in[0] = s;
+  }
+  __syncthreads();
+  if (!tree_reduce<OpSum>(tree, 1, s_in, s_out)) return;
+  if (threadIdx.x == 0) totals[2] = s_out[0];
+}
+
+// q_e = sqrt(max(2 kappa_max - kappa_e, 0)) + 1 -> pe[e]; sum -> totals[3]
+__global__ __launch_bounds__(kBlock) void k_edge_w(const double* __restrict__ kappa, int64_t m,
+                                                   Tree tree, double* totals,
+                                                   double* __restrict__ pe) {
+  __shared__ double s_w[kWavesPerBlock];
+  __shared__ double s_in[1], s_out[1];
+  const double kmax = totals[1];
+  double acc = 0.0;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < m;
+       e += static_cast<int64_t>(gridDim.x) * kBlock) {
+    const double q = sqrt(fmax(2.0 * kmax - kappa[e], 0.0)) + 1.0;
+    pe[e] = q;
+    acc += q;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = s_w[0];
+    for (int w = 1; w < kWavesPerBlock; ++w) s += s_w[w];
+    s_in[0] = s;
+  }
+  __syncthreads();
+  if (!tree_reduce<OpSum>(tree, 1, s_in, s_out)) return;
+  if (threadIdx.x == 0) totals[3] = s_out[0];
+}
+
+__global__ __launch_bounds__(kBlock) void k_normalise(DevGraph g, const double* totals,
+                                                      double inv_nonisolated,
+                                                      double* __restrict__ pn,
+                                                      double* __restrict__ pe) {
+  const double tn = totals[2];
+  const double te = totals[3];
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < g.n; i += stride) {
+    if (tn > 0.0) {
+      pn[i] = pn[i] / tn;
+    } else {
+      pn[i] = (g.rowptr[i + 1] > g.rowptr[i]) ? inv_nonisolated : 0.0;
+    }
+  }
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < g.m; e += stride)
+    pe[e] = pe[e] / te;
+}
+
+// ---------------------------------------------------------------------------------
+int grid_for(int64_t items, int64_t per_block, int cap) {
+  int64_t g = (items + per_block - 1) / per_block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return static_cast<int>(g);
+}
+
+}  // namespace
+
+// ---- launchers --------------------------------------------------------------------
+// The stream argument of hipLaunchKernelGGL is passed through a small wrapper so every
+// launch lands on the caller's stream.
+#define ERC_LAUNCH(kernel, grid, stream, ...) \
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(kBlock), 0, stream, __VA_ARGS__)
+
+hipError_t launch_fill_u32(uint32_t* p, uint32_t v, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  ERC_LAUNCH(k_fill_u32, grid_for(count, kBlock, 4096), s, p, v, count);
+  return hipGetLastError();
+}
+hipError_t launch_fill_f64(double* p, double v, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  ERC_LAUNCH(k_fill_f64, grid_for(count, kBlock, 4096), s, p, v, count);
+  return hipGetLastError();
+}
+
+template <typename T, int KB>
+static hipError_t rhs_t(const RhsArgs& a, int grid, hipStream_t s) {
+  ERC_LAUNCH((k_rhs<T, KB>), grid, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int col0, int ncols,
+                      uint64_t base, double inv_sqrt_k, double tol, hipStream_t s) {
+  RhsArgs a;
+  a.g = g;
+  a.z = w.z;
+  a.r = w.r;
+  a.p = w.p;
+  a.col0 = col0;
+  a.ncols = ncols;
+  a.words = static_cast<uint64_t>((K + 63) / 64);
+  a.base = base;
+  a.inv_sqrt_k = inv_sqrt_k;
+  a.tol2 = tol * tol;
+  a.tree = w.tree;
+  a.cs = w.cs;
+  const int grid = w.grid_rhs;
+  if (dt == ERC_F32) {
+    switch (w.kb) {
+      case 16: return rhs_t<float, 16>(a, grid, s);
+      case 32: return rhs_t<float, 32>(a, grid, s);
+      case 64: return rhs_t<float, 64>(a, grid, s);
+      case 128: return rhs_t<float, 128>(a, grid, s);
+      case 256: return rhs_t<float, 256>(a, grid, s);
+    }
+  } else {
+    switch (w.kb) {
+      case 8: return rhs_t<double, 8>(a, grid, s);
+      case 16: return rhs_t<double, 16>(a, grid, s);
+      case 32: return rhs_t<double, 32>(a, grid, s);
+      case 64: return rhs_t<double, 64>(a, grid, s);
+      case 128: return rhs_t<double, 128>(a, grid, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int LPN>
+static hipError_t spmm_launch(const SpmmArgs& a, hipStream_t s) {
+  if (a.g.weighted)
+    ERC_LAUNCH((k_spmm<T, LPN, true>), a.g.grid, s, a);
+  else
+    ERC_LAUNCH((k_spmm<T, LPN, false>), a.g.grid, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double delta, const void* p,
+                       const void* r, void* q, const int32_t* gate, hipStream_t s) {
+  SpmmArgs a;
+  a.g = g;
+  a.p = p;
+  a.r = r;
+  a.q = q;
+  a.chunkbuf = w.chunkbuf;
+  a.mega_dots = w.mega_dots;
+  a.mega_tick = w.mega_tick;
+  a.tree = w.tree;
+  a.cs = w.cs;
+  a.gate = gate;
+  a.delta = delta;
+  a.finalise = (gate == w.cs.n_active) ? 1 : 0;
+  const int lpn = (dt == ERC_F32) ? w.kb / 4 : w.kb / 2;
+  if (dt == ERC_F32) {
+    switch (lpn) {
+      case 4: return spmm_launch<float, 4>(a, s);
+      case 8: return spmm_launch<float, 8>(a, s);
+      case 16: return spmm_launch<float, 16>(a, s);
+      case 32: return spmm_launch<float, 32>(a, s);
+      case 64: return spmm_launch<float, 64>(a, s);
+    }
+  } else {
+    switch (lpn) {
+      case 4: return spmm_launch<double, 4>(a, s);
+      case 8: return spmm_launch<double, 8>(a, s);
+      case 16: return spmm_launch<double, 16>(a, s);
+      case 32: return spmm_launch<double, 32>(a, s);
+      case 64: return spmm_launch<double, 64>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int CG>
+static hipError_t upd_launch(const UpdArgs& a, int grid, hipStream_t s) {
+  ERC_LAUNCH((k_update<T, CG>), grid, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStream_t s) {
+  UpdArgs a;
+  a.z = w.z;
+  a.r = w.r;
+  a.p = w.p;
+  a.q = w.q;
+  const int vec = (dt == ERC_F32) ? 4 : 2;
+  a.nvec = static_cast<int64_t>(g.n) * w.kb / vec;
+  a.tree = w.tree;
+  a.cs = w.cs;
+  const int cg = w.kb / vec;
+  const int grid = w.grid_upd;
+  if (dt == ERC_F32) {
+    switch (cg) {
+      case 4: return upd_launch<float, 4>(a, grid, s);
+      case 8: return upd_launch<float, 8>(a, grid, s);
+      case 16: return upd_launch<float, 16>(a, grid, s);
+      case 32: return upd_launch<float, 32>(a, grid, s);
+      case 64: return upd_launch<float, 64>(a, grid, s);
+    }
+  } else {
+    switch (cg) {
+      case 4: return upd_launch<double, 4>(a, grid, s);
+      case 8: return upd_launch<double, 8>(a, grid, s);
+      case 16: return upd_launch<double, 16>(a, grid, s);
+      case 32: return upd_launch<double, 32>(a, grid, s);
+      case 64: return upd_launch<double, 64>(a, grid, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T, int LPN>
+static hipError_t ed_launch(const DevGraph& g, const void* z, double* R, int acc, int grid,
+                            hipStream_t s) {
+  ERC_LAUNCH((k_edge_dist<T, LPN>), grid, s, g, static_cast<const T*>(z), R, acc);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_dist(const DevGraph& g, const Work& w, erc_dtype dt, double* R,
+                            int accumulate, hipStream_t s) {
+  if (g.npiece == 0) return hipSuccess;
+  const int lpn = (dt == ERC_F32) ? w.kb / 4 : w.kb / 2;
+  const int grid = w.grid_ed;
+  if (dt == ERC_F32) {
+    switch (lpn) {
+      case 4: return ed_launch<float, 4>(g, w.z, R, accumulate, grid, s);
+      case 8: return ed_launch<float, 8>(g, w.z, R, accumulate, grid, s);
+      case 16: return ed_launch<float, 16>(g, w.z, R, accumulate, grid, s);
+      case 32: return ed_launch<float, 32>(g, w.z, R, accumulate, grid, s);
+      case 64: return ed_launch<float, 64>(g, w.z, R, accumulate, grid, s);
+    }
+  } else {
+    switch (lpn) {
+      case 4: return ed_launch<double, 4>(g, w.z, R, accumulate, grid, s);
+      case 8: return ed_launch<double, 8>(g, w.z, R, accumulate, grid, s);
+      case 16: return ed_launch<double, 16>(g, w.z, R, accumulate, grid, s);
+      case 32: return ed_launch<double, 32>(g, w.z, R, accumulate, grid, s);
+      case 64: return ed_launch<double, 64>(g, w.z, R, accumulate, grid, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_count_bad(const double* x, int64_t count, const Work& w, hipStream_t s) {
+  const int grid = grid_for(count, kBlock * 16, 2048);
+  ERC_LAUNCH(k_count_bad, grid, s, x, count, w.tree, w.out);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_cols(const DevGraph& g, const void* src, int kb, erc_dtype dt, int ncols,
+                            void* dst, hipStream_t s) {
+  const int64_t total = static_cast<int64_t>(g.n) * ncols;
+  if (total == 0) return hipSuccess;
+  const int grid = grid_for(total, kBlock * 4, 8192);
+  if (dt == ERC_F32)
+    ERC_LAUNCH((k_copy_cols<float>), grid, s, static_cast<const float*>(src), kb,
+               static_cast<float*>(dst), ncols, static_cast<int64_t>(g.n));
+  else
+    ERC_LAUNCH((k_copy_cols<double>), grid, s, static_cast<const double*>(src), kb,
+               static_cast<double*>(dst), ncols, static_cast<int64_t>(g.n));
+  return hipGetLastError();
+}
+
+hipError_t launch_node_p(const DevGraph& g, erc_dtype dt, const double* R, double* p,
+                         hipStream_t s) {
+  const int grid = grid_for(g.n, kWavesPerBlock, 8192);
+  if (dt == ERC_F32)
+    ERC_LAUNCH(k_node_p<float>, grid, s, g, R, p);
+  else
+    ERC_LAUNCH(k_node_p<double>, grid, s, g, R, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_edge_kappa(const DevGraph& g, const double* R, const double* p, double* kappa,
+                             hipStream_t s) {
+  if (g.npiece == 0) return hipSuccess;
+  const int grid = grid_for(g.npiece, kWavesPerBlock, 8192);
+  ERC_LAUNCH(k_edge_kappa, grid, s, g, R, p, kappa);
+  return hipGetLastError();
+}
+
+hipError_t launch_endpoints(const DevGraph& g, int32_t* u, int32_t* v, hipStream_t s) {
+  if (g.npiece == 0) return hipSuccess;
+  const int grid = grid_for(g.npiece, kWavesPerBlock, 8192);
+  ERC_LAUNCH(k_endpoints, grid, s, g, u, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_eids(const DevGraph& g, int32_t* out, hipStream_t s) {
+  if (g.nnz == 0) return hipSuccess;
+  return hipMemcpyAsync(out, g.eid, g.nnz * sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+}
+
+hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,
+                           const SampleWork& sw, double* pn, double* pe, hipStream_t s) {
+  const int grid = sw.grid;
+  ERC_LAUNCH(k_minmax, grid, s, kappa, g.m, sw.tree, sw.totals);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const int gn = grid_for(g.n, kWavesPerBlock * 8, sw.grid);
+  // the node-weight tree needs its own grid size; reuse the same scratch (stream order)
+  ERC_LAUNCH(k_node_w, gn, s, g, kappa, eta, sw.tree, sw.totals, pn);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  ERC_LAUNCH(k_edge_w, grid, s, kappa, g.m, sw.tree, sw.totals, pe);
+  if ((err = hipGetLastError()) != hipSuccess) return err;
+  const double inv = nonisolated > 0 ? 1.0 / static_cast<double>(nonisolated) : 0.0;
+  const int gz = grid_for(g.n > g.m ? g.n : g.m, kBlock * 4, 4096);
+  ERC_LAUNCH(k_normalise, gz, s, g, sw.totals, inv, pn, pe);
+  return hipGetLastError();
+}
+
+}  // namespace erc
