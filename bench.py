@@ -109,6 +109,9 @@ def main() -> int:
     ap.add_argument("--config", default="cl2400k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-iters", type=int, default=1)
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the timed steps, copy a buffer of this size 3 times (a plain "
+                         "copy kernel of known size, to calibrate HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the column "
@@ -171,6 +174,16 @@ def main() -> int:
                 "kernel": "k_spmm", "bytes_per_launch": bytes_launch,
                 "avg_launch_ms": round(avg_spmm_ms, 4), "launches": spmm_n}
     iters_total = infos[-1]["iters_total"]
+
+    if args.copy_probe_mib > 0:
+        nb = args.copy_probe_mib << 20
+        src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)  # an elementwise kernel: reads nb bytes, writes nb
+        torch.cuda.synchronize()
+        log(f"copy probe: 3 x {nb} bytes read + written")
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -15,8 +15,10 @@ constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / 64;
 // Fan-in of one level of the deterministic grid reduction tree.
 constexpr int kTreeFan = 32;
-// Largest grid a reduced kernel may use (three tree levels of 32).
-constexpr int kMaxGrid = kTreeFan * kTreeFan * kTreeFan;
+// Largest grid of a kernel whose block partials are reduced by a finishing launch.
+constexpr int kMaxGrid = 8192;
+// Largest grid of a launch that reduces through the ticket tree directly.
+constexpr int kMaxTreeGrid = 2048;
 
 // Device view of the graph operator (all pointers are device memory inside the
 // caller's graph buffer).
@@ -87,8 +89,9 @@ struct Work {
   double* mega_dots; // nmega x 3 x kb compensated (s, c) pairs
   uint32_t* mega_tick;  // nmega counters
   ColState cs;
-  Tree tree;
-  double* out;       // small fp64 output area (totals for the host, kb * 4)
+  double* part;      // block partials of the last reduced launch: grid x 3 x kb pairs
+  Tree tree;         // tickets and levels of the small finishing launches
+  double* out;       // small fp64 output area (totals for the host)
   int32_t grid_rhs, grid_upd, grid_ed;
 };
 

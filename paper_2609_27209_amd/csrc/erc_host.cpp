@@ -40,7 +40,7 @@ constexpr int64_t kPiece = 1024;
 constexpr int kMaxGridRhs = 8192;
 constexpr int kMaxGridUpd = 8192;
 constexpr int kMaxGridEd = 8192;
-constexpr int kCountBadGrid = 2048;
+constexpr int kCountBadGrid = kMaxTreeGrid;
 constexpr int kSampleGrid = 2048;
 constexpr int kDefaultCheck = 16;
 
@@ -305,7 +305,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 // Workspace layout for a padded block width.
 struct WorkLayout {
   int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rho0, thr, alpha, beta, active,
-      iters, status, n_active, one, lvl0, lvl1, lvl2, tick, out, total;
+      iters, status, n_active, one, part, lvl0, lvl1, lvl2, tick, out, total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
 };
 
@@ -344,7 +344,7 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   const int64_t nvec = h->n * kb / vec;
   L.grid_upd = static_cast<int>(std::min<int64_t>(kMaxGridUpd, std::max<int64_t>(1, ceil_div(nvec, kBlock * 4))));
   L.grid_ed = static_cast<int>(std::min<int64_t>(kMaxGridEd, std::max<int64_t>(1, ceil_div(h->dg.npiece, kWavesPerBlock))));
-  L.grid_tree = std::max({h->dg.grid, L.grid_rhs, L.grid_upd, kCountBadGrid});
+  L.grid_tree = std::max({h->dg.grid, L.grid_rhs, L.grid_upd});
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
     const int64_t at = off;
@@ -370,10 +370,12 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.n_active = take(4);
   L.one = take(4);
   const int64_t nval = 6 * kb;  // three compensated (s, c) pairs per column
-  L.lvl0 = take(static_cast<int64_t>(L.grid_tree) * nval * 8);
-  L.lvl1 = take(ceil_div(L.grid_tree, kTreeFan) * nval * 8);
-  L.lvl2 = take(ceil_div(L.grid_tree, kTreeFan * kTreeFan) * nval * 8);
-  L.tick = take(tree_ticks(L.grid_tree) * 4);
+  L.part = take(static_cast<int64_t>(L.grid_tree) * nval * 8);
+  // the finishing launches run ceil(grid/32) <= 256 blocks; k_count_bad runs <= 2048
+  L.lvl0 = take(static_cast<int64_t>(kMaxTreeGrid) * nval * 8);
+  L.lvl1 = take(ceil_div(kMaxTreeGrid, kTreeFan) * nval * 8);
+  L.lvl2 = take(ceil_div(kMaxTreeGrid, kTreeFan * kTreeFan) * nval * 8);
+  L.tick = take(tree_ticks(kMaxTreeGrid) * 4);
   L.out = take(8 * 8);
   L.total = off;
   return L;
@@ -400,6 +402,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
   w.cs.status = reinterpret_cast<int32_t*>(b + L.status);
   w.cs.n_active = reinterpret_cast<int32_t*>(b + L.n_active);
   w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
+  w.part = reinterpret_cast<double*>(b + L.part);
   w.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
   w.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
   w.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
@@ -414,7 +417,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
 // Zero the tickets and set the constant-one gate (fill kernels, so a captured stream
 // records no memset node).
 erc_status prepare_work(const erc_graph_s* h, const Work& w, const WorkLayout& L, hipStream_t s) {
-  ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(L.grid_tree), s));
+  ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(kMaxTreeGrid), s));
   ERC_HIP(launch_fill_u32(w.mega_tick, 0u, h->dg.nmega, s));
   ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.one), 1u, 1, s));
   return ERC_OK;

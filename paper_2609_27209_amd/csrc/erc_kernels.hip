@@ -241,8 +241,11 @@ __device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
 // ---------------------------------------------------------------------------------
 // Neighbour gather of one row range: acc += w_ij (p_i - p_j) over CSR entries
 // [beg, end) of row i.  Lane (grp, sub) handles neighbour slot grp of each step and
-// columns [sub*VEC, sub*VEC + VEC).  Slots past the end read p_i (weight 0), which
-// adds exactly zero, so the loop has no per-load predicate.
+// columns [sub*VEC, sub*VEC + VEC).  Each lane issues kInflight row loads before it
+// consumes them, so a wavefront keeps kInflight * 1 KB of gathers in flight.  Slots past
+// the end read p_i with weight 0, which adds exactly zero.
+constexpr int kInflight = 4;
+
 template <typename T, int LPN, bool W>
 __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
                                            const T* __restrict__ wgt, const T* __restrict__ P,
@@ -262,18 +265,29 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
       if (W) myw = __builtin_nontemporal_load(wgt + base + lane);
     }
     const int steps = (cnt + NPW - 1) / NPW;
-#pragma unroll 4
-    for (int st = 0; st < steps; ++st) {
-      const int k = st * NPW + grp;
-      const int j = __shfl(myj, k);
-      const V<T> pj = ldv(P + static_cast<int64_t>(j) * KB + sub * VEC);
-      if (W) {
-        const T wj = __shfl(myw, k);
+    for (int st = 0; st < steps; st += kInflight) {
+      V<T> pj[kInflight];
+      T wj[kInflight];
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) acc.x[v] += wj * (pi.x[v] - pj.x[v]);
-      } else {
+      for (int u = 0; u < kInflight; ++u) {
+        const int k = (st + u) * NPW + grp;
+        int j = __shfl(myj, k & 63);
+        wj[u] = W ? __shfl(myw, k & 63) : T(1);
+        if (k >= cnt) {
+          j = i;
+          wj[u] = T(0);
+        }
+        pj[u] = ldv(P + static_cast<int64_t>(j) * KB + sub * VEC);
+      }
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) acc.x[v] += pi.x[v] - pj.x[v];
+      for (int u = 0; u < kInflight; ++u) {
+        if (W) {
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc.x[v] += wj[u] * (pi.x[v] - pj[u].x[v]);
+        } else {
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc.x[v] += pi.x[v] - pj[u].x[v];
+        }
       }
     }
   }
@@ -298,11 +312,9 @@ struct SpmmArgs {
   void* chunkbuf;
   double* mega_dots;  // nmega x 3 x kb pairs
   uint32_t* mega_tick;
-  Tree tree;
-  ColState cs;
+  double* part;       // grid x 3 x kb pairs: this launch's block partials
   const int32_t* gate;
   double delta;
-  int finalise;  // 1: compute alpha, beta from the dot products
 };
 
 // q = (L + delta I) p for a block of kb = LPN*VEC columns, plus per-column p.q, r.q,
@@ -441,16 +453,54 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
     s_dots[0][v] = acc;
   }
   __syncthreads();
-  DDv* s_out = s_dots[1];
-  if (!tree_sum_dd(a.tree, 3 * KB, s_dots[0], s_out)) return;
-  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
-  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
+  DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * 3 * KB;
+  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) part[v] = s_dots[0][v];
+}
+
+// Level-1 sum of the block partials written by the previous launch: block b of this
+// small grid adds partials [32 b, 32 b + 32) in order; the blocks then meet in the
+// ticket tree.  Reading the partials in a separate launch makes them visible without a
+// device-scope fence in every block of the large kernel.  Returns true in the block
+// that holds the totals (`out`, LDS).
+__device__ bool reduce_partials(const DDv* __restrict__ part, int nparts, int nval,
+                                const Tree& t, DDv* in, DDv* out) {
+  const int b0 = blockIdx.x * kTreeFan;
+  const int nb = min(kTreeFan, nparts - b0);
+  for (int v = threadIdx.x; v < nval; v += blockDim.x) {
+    DDv acc = part[static_cast<int64_t>(b0) * nval + v];
+    for (int k = 1; k < nb; ++k) acc = dd_add(acc, part[static_cast<int64_t>(b0 + k) * nval + v]);
+    in[v] = acc;
+  }
+  __syncthreads();
+  return tree_sum_dd(t, nval, in, out);
+}
+
+struct FinArgs {
+  const double* part;
+  int nparts;        // blocks of the launch that wrote `part`
+  Tree tree;
+  ColState cs;
+  const double* mega_dots;
+  int nmega;
+  const int32_t* gate;
+  double tol2;       // (k_fin_rhs)
+  int ncols;         // (k_fin_rhs)
+};
+
+// alpha, beta of every active column from p.q, r.q, q.q (SpMM partials + long rows).
+template <int KB>
+__global__ __launch_bounds__(kBlock) void k_fin_spmm(FinArgs a) {
+  if (*a.gate == 0) return;
+  __shared__ DDv s_in[3 * KB];
+  __shared__ DDv s_out[3 * KB];
+  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, 3 * KB, a.tree, s_in, s_out))
+    return;
+  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
     DDv acc = s_out[v];
-    for (int mh = 0; mh < a.g.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
+    for (int mh = 0; mh < a.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
     s_out[v] = acc;
   }
   __syncthreads();
-  if (!a.finalise) return;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     if (a.cs.active[c]) {
       const double pq = dd_value(s_out[c]);
@@ -486,7 +536,7 @@ struct UpdArgs {
   void* p;
   const void* q;
   int64_t nvec;  // n * kb / VEC
-  Tree tree;
+  double* part;  // grid x kb pairs
   ColState cs;
 };
 
@@ -500,8 +550,6 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
   static_assert(kBlock % CG == 0, "column groups must divide the block");
   if (*a.cs.n_active == 0) return;
   __shared__ DDv s_part[kBlock][VEC];
-  __shared__ DDv s_in[KB];
-  __shared__ DDv s_out[KB];
   const int cg = threadIdx.x % CG;
   T al[VEC], be[VEC];
   bool act[VEC];
@@ -536,14 +584,23 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
 #pragma unroll
   for (int v = 0; v < VEC; ++v) s_part[threadIdx.x][v] = part[v].get();
   __syncthreads();
+  DDv* bp = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * KB;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     const int g = c / VEC, v = c % VEC;
     DDv acc = s_part[g][v];
     for (int t = g + CG; t < kBlock; t += CG) acc = dd_add(acc, s_part[t][v]);
-    s_in[c] = acc;
+    bp[c] = acc;
   }
-  __syncthreads();
-  if (!tree_sum_dd(a.tree, KB, s_in, s_out)) return;
+}
+
+// rho' = r.r of every active column; iteration count, stopping test, active count.
+template <int KB>
+__global__ __launch_bounds__(kBlock) void k_fin_update(FinArgs a) {
+  if (*a.cs.n_active == 0) return;
+  __shared__ DDv s_in[KB];
+  __shared__ DDv s_out[KB];
+  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, KB, a.tree, s_in, s_out))
+    return;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     if (a.cs.active[c]) {
       const double rn = dd_value(s_out[c]);
@@ -573,9 +630,7 @@ struct RhsArgs {
   uint64_t words;  // 64-bit sign words per edge, ceil(K/64)
   uint64_t base;   // SplitMix64 state the sign stream starts from
   double inv_sqrt_k;
-  double tol2;
-  Tree tree;
-  ColState cs;
+  double* part;    // grid x kb pairs
 };
 
 // One wavefront per row; lane l holds columns l, l+64, ... of the block.  The sum over
@@ -655,8 +710,17 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
     s_part[0][c] = acc;
   }
   __syncthreads();
-  DDv* s_out = s_part[1];
-  if (!tree_sum_dd(a.tree, KB, s_part[0], s_out)) return;
+  DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * KB;
+  for (int c = threadIdx.x; c < KB; c += kBlock) part[c] = s_part[0][c];
+}
+
+// rho_0 = y.y per column; initial CG state of the block.
+template <int KB>
+__global__ __launch_bounds__(kBlock) void k_fin_rhs(FinArgs a) {
+  __shared__ DDv s_in[KB];
+  __shared__ DDv s_out[KB];
+  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, KB, a.tree, s_in, s_out))
+    return;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     const double rr = dd_value(s_out[c]);
     a.cs.rho[c] = rr;
@@ -979,10 +1043,69 @@ hipError_t launch_fill_f64(double* p, double v, int64_t count, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int KB>
+static hipError_t fin_launch(int which, const FinArgs& f, hipStream_t s) {
+  const int grid = (f.nparts + kTreeFan - 1) / kTreeFan;
+  if (which == 0)
+    ERC_LAUNCH((k_fin_rhs<KB>), grid, s, f);
+  else if (which == 1)
+    ERC_LAUNCH((k_fin_spmm<KB>), grid, s, f);
+  else
+    ERC_LAUNCH((k_fin_update<KB>), grid, s, f);
+  return hipGetLastError();
+}
+
+static hipError_t fin_dispatch(int which, int kb, const FinArgs& f, hipStream_t s) {
+  switch (kb) {
+    case 8: return fin_launch<8>(which, f, s);
+    case 16: return fin_launch<16>(which, f, s);
+    case 32: return fin_launch<32>(which, f, s);
+    case 64: return fin_launch<64>(which, f, s);
+    case 128: return fin_launch<128>(which, f, s);
+    case 256: return fin_launch<256>(which, f, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+static FinArgs fin_args(const Work& w, int nparts) {
+  FinArgs f;
+  f.part = w.part;
+  f.nparts = nparts;
+  f.tree = w.tree;
+  f.cs = w.cs;
+  f.mega_dots = w.mega_dots;
+  f.nmega = 0;
+  f.gate = w.cs.n_active;
+  f.tol2 = 0.0;
+  f.ncols = 0;
+  return f;
+}
+
 template <typename T, int KB>
 static hipError_t rhs_t(const RhsArgs& a, int grid, hipStream_t s) {
   ERC_LAUNCH((k_rhs<T, KB>), grid, s, a);
   return hipGetLastError();
+}
+
+static hipError_t rhs_dispatch(erc_dtype dt, int kb, const RhsArgs& a, int grid, hipStream_t s) {
+  if (dt == ERC_F32) {
+    switch (kb) {
+      case 16: return rhs_t<float, 16>(a, grid, s);
+      case 32: return rhs_t<float, 32>(a, grid, s);
+      case 64: return rhs_t<float, 64>(a, grid, s);
+      case 128: return rhs_t<float, 128>(a, grid, s);
+      case 256: return rhs_t<float, 256>(a, grid, s);
+    }
+  } else {
+    switch (kb) {
+      case 8: return rhs_t<double, 8>(a, grid, s);
+      case 16: return rhs_t<double, 16>(a, grid, s);
+      case 32: return rhs_t<double, 32>(a, grid, s);
+      case 64: return rhs_t<double, 64>(a, grid, s);
+      case 128: return rhs_t<double, 128>(a, grid, s);
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int col0, int ncols,
@@ -997,28 +1120,13 @@ hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int
   a.words = static_cast<uint64_t>((K + 63) / 64);
   a.base = base;
   a.inv_sqrt_k = inv_sqrt_k;
-  a.tol2 = tol * tol;
-  a.tree = w.tree;
-  a.cs = w.cs;
-  const int grid = w.grid_rhs;
-  if (dt == ERC_F32) {
-    switch (w.kb) {
-      case 16: return rhs_t<float, 16>(a, grid, s);
-      case 32: return rhs_t<float, 32>(a, grid, s);
-      case 64: return rhs_t<float, 64>(a, grid, s);
-      case 128: return rhs_t<float, 128>(a, grid, s);
-      case 256: return rhs_t<float, 256>(a, grid, s);
-    }
-  } else {
-    switch (w.kb) {
-      case 8: return rhs_t<double, 8>(a, grid, s);
-      case 16: return rhs_t<double, 16>(a, grid, s);
-      case 32: return rhs_t<double, 32>(a, grid, s);
-      case 64: return rhs_t<double, 64>(a, grid, s);
-      case 128: return rhs_t<double, 128>(a, grid, s);
-    }
-  }
-  return hipErrorInvalidValue;
+  a.part = w.part;
+  hipError_t e = rhs_dispatch(dt, w.kb, a, w.grid_rhs, s);
+  if (e != hipSuccess) return e;
+  FinArgs f = fin_args(w, w.grid_rhs);
+  f.tol2 = tol * tol;
+  f.ncols = ncols;
+  return fin_dispatch(0, w.kb, f, s);
 }
 
 template <typename T, int LPN>
@@ -1040,30 +1148,32 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
   a.chunkbuf = w.chunkbuf;
   a.mega_dots = w.mega_dots;
   a.mega_tick = w.mega_tick;
-  a.tree = w.tree;
-  a.cs = w.cs;
+  a.part = w.part;
   a.gate = gate;
   a.delta = delta;
-  a.finalise = (gate == w.cs.n_active) ? 1 : 0;
   const int lpn = (dt == ERC_F32) ? w.kb / 4 : w.kb / 2;
+  hipError_t e = hipErrorInvalidValue;
   if (dt == ERC_F32) {
     switch (lpn) {
-      case 4: return spmm_launch<float, 4>(a, s);
-      case 8: return spmm_launch<float, 8>(a, s);
-      case 16: return spmm_launch<float, 16>(a, s);
-      case 32: return spmm_launch<float, 32>(a, s);
-      case 64: return spmm_launch<float, 64>(a, s);
+      case 4: e = spmm_launch<float, 4>(a, s); break;
+      case 8: e = spmm_launch<float, 8>(a, s); break;
+      case 16: e = spmm_launch<float, 16>(a, s); break;
+      case 32: e = spmm_launch<float, 32>(a, s); break;
+      case 64: e = spmm_launch<float, 64>(a, s); break;
     }
   } else {
     switch (lpn) {
-      case 4: return spmm_launch<double, 4>(a, s);
-      case 8: return spmm_launch<double, 8>(a, s);
-      case 16: return spmm_launch<double, 16>(a, s);
-      case 32: return spmm_launch<double, 32>(a, s);
-      case 64: return spmm_launch<double, 64>(a, s);
+      case 4: e = spmm_launch<double, 4>(a, s); break;
+      case 8: e = spmm_launch<double, 8>(a, s); break;
+      case 16: e = spmm_launch<double, 16>(a, s); break;
+      case 32: e = spmm_launch<double, 32>(a, s); break;
+      case 64: e = spmm_launch<double, 64>(a, s); break;
     }
   }
-  return hipErrorInvalidValue;
+  if (e != hipSuccess || gate != w.cs.n_active) return e;  // debug launches stop here
+  FinArgs f = fin_args(w, g.grid);
+  f.nmega = g.nmega;
+  return fin_dispatch(1, w.kb, f, s);
 }
 
 template <typename T, int CG>
@@ -1080,28 +1190,30 @@ hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStre
   a.q = w.q;
   const int vec = (dt == ERC_F32) ? 4 : 2;
   a.nvec = static_cast<int64_t>(g.n) * w.kb / vec;
-  a.tree = w.tree;
+  a.part = w.part;
   a.cs = w.cs;
   const int cg = w.kb / vec;
   const int grid = w.grid_upd;
+  hipError_t e = hipErrorInvalidValue;
   if (dt == ERC_F32) {
     switch (cg) {
-      case 4: return upd_launch<float, 4>(a, grid, s);
-      case 8: return upd_launch<float, 8>(a, grid, s);
-      case 16: return upd_launch<float, 16>(a, grid, s);
-      case 32: return upd_launch<float, 32>(a, grid, s);
-      case 64: return upd_launch<float, 64>(a, grid, s);
+      case 4: e = upd_launch<float, 4>(a, grid, s); break;
+      case 8: e = upd_launch<float, 8>(a, grid, s); break;
+      case 16: e = upd_launch<float, 16>(a, grid, s); break;
+      case 32: e = upd_launch<float, 32>(a, grid, s); break;
+      case 64: e = upd_launch<float, 64>(a, grid, s); break;
     }
   } else {
     switch (cg) {
-      case 4: return upd_launch<double, 4>(a, grid, s);
-      case 8: return upd_launch<double, 8>(a, grid, s);
-      case 16: return upd_launch<double, 16>(a, grid, s);
-      case 32: return upd_launch<double, 32>(a, grid, s);
-      case 64: return upd_launch<double, 64>(a, grid, s);
+      case 4: e = upd_launch<double, 4>(a, grid, s); break;
+      case 8: e = upd_launch<double, 8>(a, grid, s); break;
+      case 16: e = upd_launch<double, 16>(a, grid, s); break;
+      case 32: e = upd_launch<double, 32>(a, grid, s); break;
+      case 64: e = upd_launch<double, 64>(a, grid, s); break;
     }
   }
-  return hipErrorInvalidValue;
+  if (e != hipSuccess) return e;
+  return fin_dispatch(2, w.kb, fin_args(w, grid), s);
 }
 
 template <typename T, int LPN>
