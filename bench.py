@@ -22,6 +22,19 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 
+# HBM traffic of one full SpMM launch on the 2.4M-node workload, from two rocprofv3
+# --pmc runs of this benchmark (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, median
+# over full launches), each scaled by what the counter reads for a plain 1 GiB copy
+# kernel run in the same process (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for
+# the kernel source it was measured on: reported as null once that file changes.
+MEASURED_TRAFFIC = {
+    "workload": "cl2400k",
+    "kernel_sha256_16": "4d967d41617a722b",
+    "fetch_bytes": 33616574706,
+    "write_bytes": 639565824,
+    "profile": "profiles/k_spmm_cl2400k.md",
+}
+
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -35,6 +48,14 @@ def spmm_bytes_per_launch(g, kb: int, dtype: str) -> int:
     return per_nnz * g.nnz + 8 * (g.n + 1) + 3 * s * g.n * kb
 
 
+def kernel_source_hash() -> str:
+    import hashlib
+
+    path = os.path.join(ROOT, "paper_2609_27209_amd", "csrc", "erc_kernels.hip")
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
 def padded(kb: int, dtype: str) -> int:
     w = 16 if dtype == "f32" else 8
     while w < kb:
@@ -42,63 +63,62 @@ def padded(kb: int, dtype: str) -> int:
     return w
 
 
-def cpu_baseline(g, p, iters_total: int, budget_iters: int = 1):
+def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 50, cg_iters: int = 4):
     """Time the CPU oracle on a bounded sample of this workload and scale to edges/s.
 
-    Sample: the oracle's Laplacian assembly (full graph), its right-hand-side builder
-    on a random ~0.5% of the rows (one block of columns), `budget_iters` CG
-    iterations of one full block, edge distances for ~1% of the edges, and curvature
-    plus sampling on the full graph.  The full-workload time is the setup plus each
-    part scaled by its share: RHS by stored entries and blocks, CG by the column
-    iterations the GPU run took, distances by edges and blocks.
+    Sample: a 1/`scale_div` instance of the same graph recipe (n and m divided by
+    `scale_div`, the generator's offset i0 scaled with n), on which the oracle runs every
+    stage: Laplacian assembly, one block of right-hand sides, `cg_iters` CG iterations
+    of one full block, one block of edge distances, curvature and sampling.  Each stage
+    is scaled linearly in the graph size (stored entries or edges), RHS and distances by
+    the number of blocks, and CG by the column-iterations the GPU run took.
     """
     import numpy as np
 
+    import gen
     from oracle import erc as OE
     from oracle import graph as OG
 
-    rng = np.random.default_rng(0)
     kb = p.k_block
     nblocks = math.ceil(p.K / kb)
+    args = dict(wl.graph_args)
+    if wl.graph_kind == "chung_lu":
+        args.update(n=max(1000, args["n"] // scale_div), m_target=max(2000, args["m_target"] // scale_div),
+                    i0=args["i0"] / scale_div)
+        gs = gen.graphs.chung_lu(**args)
+    else:
+        gs = g
+    f_m = g.m / gs.m
+    f_nnz = g.nnz / gs.nnz
     t0 = time.perf_counter()
-    L = OG.laplacian(g)
-    eu, ev, _ = OG.canonical_edges(g)
-    t_setup = time.perf_counter() - t0
-    log(f"cpu baseline: setup {t_setup:.1f}s")
-
-    rows = np.sort(rng.choice(g.n, size=max(1, g.n // 200), replace=False))
-    ent = int(np.sum(np.diff(g.rowptr)[rows]))
+    L = OG.laplacian(gs)
+    eu, ev, _ = OG.canonical_edges(gs)
+    t_setup = (time.perf_counter() - t0) * f_m
     t0 = time.perf_counter()
-    OE.rhs(g, p.K, 0, kb, p.seed, p.dtype, rows=rows)
-    t_rhs = (time.perf_counter() - t0) * (g.nnz / max(ent, 1)) * nblocks
-    log(f"cpu baseline: rhs sample done (scaled {t_rhs:.1f}s)")
-
-    Y = rng.standard_normal((g.n, kb))
+    Y = OE.rhs(gs, p.K, 0, kb, p.seed, p.dtype)
+    t_rhs = (time.perf_counter() - t0) * f_nnz * nblocks
     t0 = time.perf_counter()
-    OE.cg_columns(L, p.delta, Y, 1e-300, budget_iters)
-    t_it = (time.perf_counter() - t0) / budget_iters
+    res = OE.cg_columns(L, p.delta, Y, 1e-300, cg_iters)
+    t_it = (time.perf_counter() - t0) / cg_iters * f_nnz
     t_cg = t_it * iters_total / kb
-    log(f"cpu baseline: {budget_iters} CG iteration(s) of {kb} columns: {t_it:.1f}s each")
-
-    Z = rng.standard_normal((g.n, kb))
-    sel = np.sort(rng.choice(g.m, size=max(1, g.m // 100), replace=False))
     t0 = time.perf_counter()
-    OE.edge_distances(Z, eu[sel], ev[sel])
-    t_dist = (time.perf_counter() - t0) * (g.m / sel.size) * nblocks
-
+    R = OE.edge_distances(res.Z, eu, ev)
+    t_dist = (time.perf_counter() - t0) * f_m * nblocks
     t0 = time.perf_counter()
-    _, kappa = OE.curvature(g, np.ones(g.m))
-    OE.sampling_probs(g, kappa, p.eta)
-    t_curv = time.perf_counter() - t0
+    _, kappa = OE.curvature(gs, R)
+    OE.sampling_probs(gs, kappa, p.eta)
+    t_curv = (time.perf_counter() - t0) * f_m
     total = t_setup + t_rhs + t_cg + t_dist + t_curv
-    sample = (f"oracle (fp64 NumPy/SciPy, single thread) on {g.n} nodes / {g.m} edges: "
-              f"Laplacian assembly {t_setup:.1f}s; RHS on 0.5% of rows x {nblocks} blocks "
-              f"({t_rhs:.1f}s scaled); {budget_iters} CG iteration of a {kb}-column block "
-              f"({t_it:.1f}s) x {iters_total} column-iterations / {kb} = {t_cg:.1f}s; edge "
-              f"distances on 1% of edges ({t_dist:.1f}s scaled); curvature + sampling full "
-              f"({t_curv:.1f}s); estimated full run {total:.1f}s")
+    log(f"cpu baseline: estimated {total:.0f}s for the full workload")
+    sample = (f"oracle (fp64 NumPy/SciPy, one thread) on a 1/{scale_div} instance of the same "
+              f"recipe ({gs.n} nodes, {gs.m} edges), scaled by edges or stored entries: "
+              f"Laplacian assembly {t_setup:.1f}s, RHS x {nblocks} blocks {t_rhs:.1f}s, CG "
+              f"{cg_iters} iterations of a {kb}-column block -> {t_it:.2f}s per iteration at "
+              f"full size x {iters_total} column-iterations / {kb} = {t_cg:.0f}s, edge "
+              f"distances {t_dist:.1f}s, curvature + sampling {t_curv:.1f}s; estimated full "
+              f"run {total:.0f}s")
     return {"value": g.m / total, "unit": "edges/s", "cores": 1, "kind": "oracle",
-            "sample": sample, "est_seconds": total}
+            "sample": sample, "est_seconds": round(total, 1)}
 
 
 def main() -> int:
@@ -108,7 +128,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="cl2400k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-iters", type=int, default=1)
+    ap.add_argument("--cpu-scale", type=int, default=50,
+                    help="the CPU baseline runs on a 1/cpu-scale instance of the workload")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this size 3 times (a plain "
                          "copy kernel of known size, to calibrate HBM byte counters)")
@@ -164,15 +185,28 @@ def main() -> int:
     value = g.m / (ms_per_step / 1000.0)
 
     kb = padded(p.k_block, p.dtype)
+    # every SpMM launch is bracketed by HIP events on the solve stream; launches that
+    # found no active column (issued before the host saw convergence) return at once,
+    # so the average is taken over the full launches
     spmm_ms = sum(i["ms_spmm"] for i in infos)
+    spmm_full = sum(i["spmm_full"] for i in infos)
     spmm_n = sum(i["spmm_timed"] for i in infos)
-    avg_spmm_ms = spmm_ms / max(spmm_n, 1)
+    avg_spmm_ms = spmm_ms / max(spmm_full, 1)
     bytes_launch = spmm_bytes_per_launch(g, kb, p.dtype)
     achieved = bytes_launch / (avg_spmm_ms / 1000.0) / 1e9
+    traffic = None
+    if (MEASURED_TRAFFIC["workload"] == args.config
+            and MEASURED_TRAFFIC["kernel_sha256_16"] == kernel_source_hash()):
+        traffic = MEASURED_TRAFFIC["fetch_bytes"] + MEASURED_TRAFFIC["write_bytes"]
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "k_spmm", "bytes_per_launch": bytes_launch,
-                "avg_launch_ms": round(avg_spmm_ms, 4), "launches": spmm_n}
+                "avg_launch_ms": round(avg_spmm_ms, 4), "launches_full": spmm_full,
+                "launches_timed": spmm_n}
+    if traffic is not None:
+        tb = traffic / (avg_spmm_ms / 1000.0) / 1e9
+        roofline["traffic_gbs"] = round(tb, 1)
+        roofline["traffic_frac"] = round(tb / PEAK_HBM_GBS, 4)
     iters_total = infos[-1]["iters_total"]
 
     if args.copy_probe_mib > 0:
@@ -188,7 +222,9 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         try:
-            cpu = cpu_baseline(g, p, iters_total, args.cpu_iters)
+            t0 = time.perf_counter()
+            cpu = cpu_baseline(g, p, wl, iters_total, args.cpu_scale)
+            cpu["sample_wall_s"] = round(time.perf_counter() - t0, 1)
         except MemoryError as exc:  # pragma: no cover - host-dependent
             log(f"cpu baseline skipped: {exc}")
 

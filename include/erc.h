@@ -128,6 +128,8 @@ typedef struct {
   float ms_total;             /* whole call, stream time                             */
   float ms_spmm;              /* with ERC_PROFILE_SPMM: summed SpMM kernel time      */
   int64_t spmm_timed;         /* with ERC_PROFILE_SPMM: SpMM launches timed          */
+  int64_t spmm_full;          /* SpMM launches that found an active column (the rest
+                                 return at once after convergence)                   */
 } erc_solve_info;
 
 /* ---- graph ---------------------------------------------------------------------- */

@@ -62,9 +62,14 @@ def sign_words(seed: int, K: int, e, word_index) -> np.ndarray:
 
 
 def signs(seed: int, K: int, e, cols) -> np.ndarray:
-    """+-1 (int8) matrix of shape (len(e), len(cols)) for global columns ``cols``."""
+    """+-1 (int8) matrix of shape (len(e), len(cols)) for global columns ``cols``.
+
+    Each sign word is generated once per edge and 64-column word, then every column
+    reads its bit from it.
+    """
     e = np.asarray(e, dtype=np.int64).reshape(-1, 1)
-    cols = np.asarray(cols, dtype=np.int64).reshape(1, -1)
-    words = sign_words(seed, K, e, cols // 64)
-    bits = (words >> (cols % 64).astype(U64)) & U64(1)
+    cols = np.asarray(cols, dtype=np.int64).reshape(-1)
+    wi, pick = np.unique(cols // 64, return_inverse=True)
+    words = sign_words(seed, K, e, wi.reshape(1, -1))[:, pick]
+    bits = (words >> (cols % 64).astype(U64).reshape(1, -1)) & U64(1)
     return (1 - 2 * bits.astype(np.int8)).astype(np.int8)

@@ -67,6 +67,7 @@ struct ColState {
   int32_t* iters;   // iterations taken
   int32_t* status;  // 0 ok, 1 breakdown
   int32_t* n_active;  // one int: number of active columns (polled by the host)
+  int32_t* upd_pending;  // one int: an update ran whose r.r is not yet reduced
   int32_t* one;       // one int holding 1 (keeps debug launches from exiting early)
 };
 
@@ -89,7 +90,8 @@ struct Work {
   double* mega_dots; // nmega x 3 x kb compensated (s, c) pairs
   uint32_t* mega_tick;  // nmega counters
   ColState cs;
-  double* part;      // block partials of the last reduced launch: grid x 3 x kb pairs
+  double* part;      // block partials of the SpMM / RHS launch: grid x 3 x kb pairs
+  double* part_u;    // block partials of the update launch: grid_upd x kb pairs
   Tree tree;         // tickets and levels of the small finishing launches
   double* out;       // small fp64 output area (totals for the host)
   int32_t grid_rhs, grid_upd, grid_ed;
@@ -104,6 +106,7 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
                        const void* p, const void* r, void* q, const int32_t* gate,
                        hipStream_t s);
 hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStream_t s);
+hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream_t s);
 hipError_t launch_edge_dist(const DevGraph& g, const Work& w, erc_dtype dt, double* R,
                             int accumulate, hipStream_t s);
 hipError_t launch_count_bad(const double* x, int64_t count, const Work& w, hipStream_t s);

@@ -305,7 +305,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 // Workspace layout for a padded block width.
 struct WorkLayout {
   int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rho0, thr, alpha, beta, active,
-      iters, status, n_active, one, part, lvl0, lvl1, lvl2, tick, out, total;
+      iters, status, n_active, upd_pending, one, part, part_u, lvl0, lvl1, lvl2, tick, out, total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
 };
 
@@ -368,9 +368,11 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.iters = take(kb * 4);
   L.status = take(kb * 4);
   L.n_active = take(4);
+  L.upd_pending = take(4);
   L.one = take(4);
-  const int64_t nval = 6 * kb;  // three compensated (s, c) pairs per column
-  L.part = take(static_cast<int64_t>(L.grid_tree) * nval * 8);
+  const int64_t nval = 8 * kb;  // up to four compensated (s, c) pairs per column
+  L.part = take(static_cast<int64_t>(L.grid_tree) * 6 * kb * 8);
+  L.part_u = take(static_cast<int64_t>(L.grid_upd) * 2 * kb * 8);
   // the finishing launches run ceil(grid/32) <= 256 blocks; k_count_bad runs <= 2048
   L.lvl0 = take(static_cast<int64_t>(kMaxTreeGrid) * nval * 8);
   L.lvl1 = take(ceil_div(kMaxTreeGrid, kTreeFan) * nval * 8);
@@ -401,8 +403,10 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
   w.cs.iters = reinterpret_cast<int32_t*>(b + L.iters);
   w.cs.status = reinterpret_cast<int32_t*>(b + L.status);
   w.cs.n_active = reinterpret_cast<int32_t*>(b + L.n_active);
+  w.cs.upd_pending = reinterpret_cast<int32_t*>(b + L.upd_pending);
   w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
   w.part = reinterpret_cast<double*>(b + L.part);
+  w.part_u = reinterpret_cast<double*>(b + L.part_u);
   w.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
   w.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
   w.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
@@ -449,7 +453,7 @@ erc_status check_params(const erc_graph_s* h, const erc_solve_params* p) {
 
 struct BlockStats {
   int32_t iters_max = 0, unconverged = 0, breakdowns = 0;
-  int64_t iters_total = 0, launches = 0;
+  int64_t iters_total = 0, launches = 0, spmm_full = 0;
   double max_relres = 0.0;
   float ms_rhs = 0, ms_cg = 0, ms_accum = 0, ms_spmm = 0;
   int64_t spmm_timed = 0;
@@ -505,6 +509,7 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
       if (prof) ERC_HIP(hipEventRecord(pr[0], s));
       ERC_HIP(launch_spmm(h->dg, w, h->dt, p->delta, w.p, w.r, w.q, w.cs.n_active, s));
       if (prof) ERC_HIP(hipEventRecord(pr[1], s));
+      ERC_HIP(launch_fin_iter(h->dg, w, 0, s));
       ERC_HIP(launch_update(h->dg, w, h->dt, s));
     }
     group_count[slot] = nb;
@@ -524,6 +529,8 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
     }
     pending = slot;
   }
+  // the last update's r.r: stopping test and iteration count of the final iteration
+  ERC_HIP(launch_fin_iter(h->dg, w, 1, s));
   ERC_HIP(hipEventRecord(h->ev[2], s));
   if (R != nullptr) ERC_HIP(launch_edge_dist(h->dg, w, h->dt, R, accumulate, s));
   ERC_HIP(hipEventRecord(h->ev[3], s));
@@ -541,6 +548,11 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
     erc_status pst = read_prof(h, pending, group_count[pending], st);
     if (pst != ERC_OK) return pst;
   }
+  int32_t block_max = 0;
+  for (int c = 0; c < nc; ++c) block_max = std::max(block_max, hb[c]);
+  // SpMM launches that found an active column: one per iteration plus the one that
+  // precedes the finishing launch which detects the last convergence
+  st->spmm_full += std::min<int64_t>(block_max + 1, done);
   for (int c = 0; c < nc; ++c) {
     const int32_t it = hb[c];
     st->iters_total += it;
@@ -852,6 +864,7 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     info->ms_total = total;
     info->ms_spmm = bs.ms_spmm;
     info->spmm_timed = bs.spmm_timed;
+    info->spmm_full = bs.spmm_full;
   }
   if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown in " + std::to_string(bs.breakdowns) + " column(s)");
   if (bad > 0) return fail(ERC_E_NUMERIC, std::to_string(bad) + " resistance(s) <= 0 or not finite");

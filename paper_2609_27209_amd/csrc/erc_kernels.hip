@@ -40,6 +40,36 @@ template <typename T>
 __device__ __forceinline__ void stv(T* p, const V<T>& v) {
   *reinterpret_cast<V<T>*>(p) = v;
 }
+// Non-temporal 16-byte loads and stores for data that is streamed once per launch, so
+// the L2 keeps the rows that neighbour gathers reuse.
+template <typename T>
+struct NtVec;
+template <>
+struct NtVec<float> {
+  typedef float type __attribute__((ext_vector_type(4)));
+};
+template <>
+struct NtVec<double> {
+  typedef double type __attribute__((ext_vector_type(2)));
+};
+template <typename T>
+__device__ __forceinline__ V<T> ldv_nt(const T* p) {
+  typedef typename NtVec<T>::type E;
+  const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
+  V<T> v;
+#pragma unroll
+  for (int k = 0; k < V<T>::N; ++k) v.x[k] = e[k];
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ void stv_nt(T* p, const V<T>& v) {
+  typedef typename NtVec<T>::type E;
+  E e;
+#pragma unroll
+  for (int k = 0; k < V<T>::N; ++k) e[k] = v.x[k];
+  __builtin_nontemporal_store(e, reinterpret_cast<E*>(p));
+}
+
 template <typename T>
 __device__ __forceinline__ V<T> vzero() {
   V<T> v;
@@ -339,23 +369,25 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
   const T* __restrict__ wgt = static_cast<const T*>(a.g.w);
   const T dlt = static_cast<T>(a.delta);
 
-  Dot<T> dpq[VEC], drq[VEC], dqq[VEC];
+  // p.q, r.q, q.q partials of the rows this lane's group finishes (block tasks are
+  // finished by group 0 of wave 0)
+  Dot<T> ldots[3 * VEC];
 
-  // finish one row in group-0 lanes: q = delta p_i + acc, store, accumulate the dots
-  // (into this lane's partials, or as this row's own pairs at `dst`)
+  // finish one row of a block task in group-0 lanes: q = delta p_i + acc, store, and
+  // accumulate the dots (into this lane's partials, or as this row's own pairs at `dst`)
   auto finish = [&](int i, const V<T>& pi, const V<T>& acc, DDv* dst) {
     V<T> qv;
+    const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
 #pragma unroll
     for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
-    const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
-    stv(Q + off, qv);
-    const V<T> ri = ldv(Rr + off);
+    stv_nt(Q + off, qv);
+    const V<T> ri = ldv_nt(Rr + off);
     if (dst == nullptr) {
 #pragma unroll
       for (int v = 0; v < VEC; ++v) {
-        dpq[v].add(pi.x[v], qv.x[v]);
-        drq[v].add(ri.x[v], qv.x[v]);
-        dqq[v].add(qv.x[v], qv.x[v]);
+        ldots[v].add(pi.x[v], qv.x[v]);
+        ldots[VEC + v].add(ri.x[v], qv.x[v]);
+        ldots[2 * VEC + v].add(qv.x[v], qv.x[v]);
       }
     } else {
 #pragma unroll
@@ -370,6 +402,7 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
   // 1. block-cooperative tasks
   for (int t = blockIdx.x; t < a.g.ntask; t += gridDim.x) {
     const int i = a.g.task_row[t];
+    const int mh = a.g.task_mega[t];
     const int64_t tb = a.g.task_beg[t];
     const int64_t len = a.g.task_end[t] - tb;
     const int64_t wb = tb + (len * wv) / kWavesPerBlock;
@@ -380,7 +413,6 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
     reduce_groups<T, LPN>(acc);
     if (lane < LPN) s_acc[wv][sub] = acc;
     __syncthreads();
-    const int mh = a.g.task_mega[t];
     V<T> tot = vzero<T>();
     if (wv == 0 && lane < LPN) {
 #pragma unroll
@@ -419,32 +451,97 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
     __syncthreads();
   }
 
-  // 2. this wave's short rows
+  // 2. this wave's short rows, NPW at a time: lane group g owns row lo + g (+ NPW ...),
+  // loads its own neighbour indices LPN at a time and gathers kInflight rows of p per
+  // step, so a wavefront has NPW rows and NPW * kInflight gathers in flight and needs
+  // no cross-group reduction per row.
   {
+    constexpr int NPW = 64 / LPN;
+    const int grp = lane / LPN;
     const int gw = blockIdx.x * kWavesPerBlock + wv;
     const int lo = a.g.wave_lo[gw];
     const int hi = a.g.wave_lo[gw + 1];
-    for (int k = lo; k < hi; ++k) {
-      const int i = a.g.light[k];
+    for (int k0 = lo; k0 < hi; k0 += NPW) {
+      const int k = k0 + grp;
+      const bool valid = k < hi;
+      const int i = valid ? a.g.light[k] : a.g.light[lo];
       const int64_t b = a.g.rowptr[i];
-      const int64_t e = a.g.rowptr[i + 1];
+      const int deg = valid ? static_cast<int>(a.g.rowptr[i + 1] - b) : 0;
       const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
       V<T> acc = vzero<T>();
-      gather_row<T, LPN, W>(a.g.col, wgt, P, i, b, e, pi, acc, lane);
-      reduce_groups<T, LPN>(acc);
-      if (lane < LPN) finish(i, pi, acc, nullptr);
+      int dmax = deg;
+#pragma unroll
+      for (int off = LPN; off < 64; off <<= 1) dmax = max(dmax, __shfl_xor(dmax, off));
+      for (int base = 0; base < dmax; base += LPN) {
+        const int t = base + sub;
+        int myj = i;
+        T myw = T(0);
+        if (t < deg) {
+          myj = __builtin_nontemporal_load(a.g.col + b + t);
+          if (W) myw = __builtin_nontemporal_load(wgt + b + t);
+        }
+        const int cnt = min(LPN, dmax - base);
+        for (int u0 = 0; u0 < cnt; u0 += kInflight) {
+          V<T> pj[kInflight];
+          T wj[kInflight];
+#pragma unroll
+          for (int u = 0; u < kInflight; ++u) {
+            const int tt = u0 + u;
+            const int src = grp * LPN + (tt & (LPN - 1));
+            int j = __shfl(myj, src);
+            wj[u] = W ? __shfl(myw, src) : T(1);
+            if (tt >= LPN || base + tt >= deg) {
+              j = i;
+              wj[u] = T(0);
+            }
+            pj[u] = ldv(P + static_cast<int64_t>(j) * KB + sub * VEC);
+          }
+#pragma unroll
+          for (int u = 0; u < kInflight; ++u) {
+            if (W) {
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) acc.x[v] += wj[u] * (pi.x[v] - pj[u].x[v]);
+            } else {
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) acc.x[v] += pi.x[v] - pj[u].x[v];
+            }
+          }
+        }
+      }
+      if (valid) {
+        const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
+        V<T> qv;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
+        stv_nt(Q + off, qv);
+        const V<T> ri = ldv_nt(Rr + off);
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+          ldots[v].add(pi.x[v], qv.x[v]);
+          ldots[VEC + v].add(ri.x[v], qv.x[v]);
+          ldots[2 * VEC + v].add(qv.x[v], qv.x[v]);
+        }
+      }
     }
   }
 
-  // 3. block partials of the three dot products (waves in order), then the grid tree
-  if (lane < LPN) {
+  // 3. block partials: fold the lane groups (xor butterfly on compensated pairs), then
+  // the waves in order, then store this block's pairs for the finishing launch
+  {
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) {
-      s_dots[wv][sub * VEC + v] = dpq[v].get();
-      s_dots[wv][KB + sub * VEC + v] = drq[v].get();
-      s_dots[wv][2 * KB + sub * VEC + v] = dqq[v].get();
+    for (int d = 0; d < 3 * VEC; ++d) {
+      DDv x = ldots[d].get();
+#pragma unroll
+      for (int off = LPN; off < 64; off <<= 1) {
+        DDv y;
+        y.s = __shfl_xor(x.s, off);
+        y.c = __shfl_xor(x.c, off);
+        x = dd_add(x, y);
+      }
+      if (lane < LPN) s_dots[wv][(d / VEC) * KB + sub * VEC + (d % VEC)] = x;
     }
   }
+
   __syncthreads();
   for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
     DDv acc = s_dots[0][v];
@@ -480,32 +577,85 @@ struct FinArgs {
   int nparts;        // blocks of the launch that wrote `part`
   Tree tree;
   ColState cs;
-  const double* mega_dots;
-  int nmega;
-  const int32_t* gate;
-  double tol2;       // (k_fin_rhs)
-  int ncols;         // (k_fin_rhs)
+  double tol2;
+  int ncols;
 };
 
-// alpha, beta of every active column from p.q, r.q, q.q (SpMM partials + long rows).
+// Level-1 sum of one set of block partials: block b of the finishing grid adds
+// partials [32 b, 32 b + 32) of the set in order (none past its end).
+__device__ void level1_sum(const DDv* __restrict__ part, int nparts, int nval, DDv* dst) {
+  const int b0 = blockIdx.x * kTreeFan;
+  const int nb = min(kTreeFan, nparts - b0);
+  for (int v = threadIdx.x; v < nval; v += blockDim.x) {
+    DDv acc = DDv{0.0, 0.0};
+    if (nb > 0) {
+      acc = part[static_cast<int64_t>(b0) * nval + v];
+      for (int k = 1; k < nb; ++k) acc = dd_add(acc, part[static_cast<int64_t>(b0 + k) * nval + v]);
+    }
+    dst[v] = acc;
+  }
+}
+
+struct IterArgs {
+  const double* part_s;  // SpMM block partials: p.q, r.q, q.q (3 kb pairs per block)
+  int nparts_s;
+  const double* part_u;  // update block partials: r.r (kb pairs per block)
+  int nparts_u;
+  Tree tree;
+  ColState cs;
+  const double* mega_dots;
+  int nmega;
+  int mode;              // 0: stopping test of the pending update, then alpha/beta; 1: test only
+};
+
+// One finishing launch per CG iteration, between the SpMM and the update kernels:
+//  (1) r.r of the update of the previous iteration (if one ran): iteration count,
+//      rho, and the per-column stopping test rho' <= tol^2 rho_0;
+//  (2) p.q, r.q, q.q of this SpMM: alpha = rho / p.q and, for the direction update,
+//      rho' = ||r - alpha q||^2 expanded in double-double.
+// Reducing the two partial sets in one tree saves a launch per iteration.
 template <int KB>
-__global__ __launch_bounds__(kBlock) void k_fin_spmm(FinArgs a) {
-  if (*a.gate == 0) return;
-  __shared__ DDv s_in[3 * KB];
-  __shared__ DDv s_out[3 * KB];
-  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, 3 * KB, a.tree, s_in, s_out))
-    return;
-  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);  for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
-    DDv acc = s_out[v];
-    for (int mh = 0; mh < a.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
-    s_out[v] = acc;
+__global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
+  if (*a.cs.n_active == 0) return;
+  __shared__ DDv s_in[4 * KB];
+  __shared__ DDv s_out[4 * KB];
+  const bool upd = *a.cs.upd_pending != 0;
+  const bool dots = a.mode == 0;
+  if (upd) {
+    level1_sum(reinterpret_cast<const DDv*>(a.part_u), a.nparts_u, KB, s_in);
+  } else {
+    for (int v = threadIdx.x; v < KB; v += kBlock) s_in[v] = DDv{0.0, 0.0};
+  }
+  if (dots) {
+    level1_sum(reinterpret_cast<const DDv*>(a.part_s), a.nparts_s, 3 * KB, s_in + KB);
+  } else {
+    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) s_in[KB + v] = DDv{0.0, 0.0};
+  }
+  __syncthreads();
+  if (!tree_sum_dd(a.tree, 4 * KB, s_in, s_out)) return;
+  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
+  if (dots) {
+    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
+      DDv acc = s_out[KB + v];
+      for (int mh = 0; mh < a.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
+      s_out[KB + v] = acc;
+    }
   }
   __syncthreads();
   for (int c = threadIdx.x; c < KB; c += kBlock) {
-    if (a.cs.active[c]) {
-      const double pq = dd_value(s_out[c]);
-      const DDv rq = s_out[KB + c];
-      const DDv qq = s_out[2 * KB + c];
+    if (upd && a.cs.active[c]) {
+      const double rn = dd_value(s_out[c]);
+      a.cs.iters[c] += 1;
+      a.cs.rho[c] = rn;
+      if (!(rn > a.cs.thr[c])) {
+        a.cs.active[c] = 0;
+        if (!isfinite(rn)) a.cs.status[c] = 1;
+      }
+    }
+    if (dots && a.cs.active[c]) {
+      const double pq = dd_value(s_out[KB + c]);
+      const DDv rq = s_out[2 * KB + c];
+      const DDv qq = s_out[3 * KB + c];
       const double rho = a.cs.rho[c];
       if (!(pq > 0.0) || !isfinite(pq) || !isfinite(dd_value(rq)) || !isfinite(dd_value(qq))) {
         a.cs.active[c] = 0;
@@ -514,8 +664,8 @@ __global__ __launch_bounds__(kBlock) void k_fin_spmm(FinArgs a) {
         a.cs.beta[c] = 0.0;
       } else {
         // rho' = ||r - alpha q||^2 = rho - 2 alpha r.q + alpha^2 q.q, evaluated in
-        // double-double; the exact r.r is recomputed by k_update and used for the
-        // stopping test and the next alpha.
+        // double-double; the exact r.r of the updated r is reduced by the next launch
+        // and drives the stopping test and the next alpha.
         const double al = rho / pq;
         const DDv t1 = dd_mul_d(rq, -2.0 * al);
         const DDv t2 = dd_mul_d(dd_mul_d(qq, al), al);
@@ -527,6 +677,13 @@ __global__ __launch_bounds__(kBlock) void k_fin_spmm(FinArgs a) {
       a.cs.alpha[c] = 0.0;
       a.cs.beta[c] = 0.0;
     }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int cnt = 0;
+    for (int c = 0; c < KB; ++c) cnt += a.cs.active[c] != 0;
+    *a.cs.n_active = cnt;
+    *a.cs.upd_pending = (dots && cnt > 0) ? 1 : 0;
   }
 }
 
@@ -568,8 +725,8 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < a.nvec; x += stride) {
     const int64_t o = x * VEC;
-    V<T> z = ldv(Z + o), r = ldv(R + o), p = ldv(P + o);
-    const V<T> q = ldv(Qv + o);
+    V<T> z = ldv_nt(Z + o), r = ldv_nt(R + o), p = ldv_nt(P + o);
+    const V<T> q = ldv_nt(Qv + o);
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
       z.x[v] += al[v] * p.x[v];
@@ -577,9 +734,9 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
       if (act[v]) p.x[v] = r.x[v] + be[v] * p.x[v];
       part[v].add(r.x[v], r.x[v]);
     }
-    stv(Z + o, z);
-    stv(R + o, r);
-    stv(P + o, p);
+    stv_nt(Z + o, z);
+    stv_nt(R + o, r);
+    stv(P + o, p);  // p is gathered by the next SpMM
   }
 #pragma unroll
   for (int v = 0; v < VEC; ++v) s_part[threadIdx.x][v] = part[v].get();
@@ -590,33 +747,6 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
     DDv acc = s_part[g][v];
     for (int t = g + CG; t < kBlock; t += CG) acc = dd_add(acc, s_part[t][v]);
     bp[c] = acc;
-  }
-}
-
-// rho' = r.r of every active column; iteration count, stopping test, active count.
-template <int KB>
-__global__ __launch_bounds__(kBlock) void k_fin_update(FinArgs a) {
-  if (*a.cs.n_active == 0) return;
-  __shared__ DDv s_in[KB];
-  __shared__ DDv s_out[KB];
-  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, KB, a.tree, s_in, s_out))
-    return;
-  for (int c = threadIdx.x; c < KB; c += kBlock) {
-    if (a.cs.active[c]) {
-      const double rn = dd_value(s_out[c]);
-      a.cs.iters[c] += 1;
-      a.cs.rho[c] = rn;
-      if (!(rn > a.cs.thr[c])) {
-        a.cs.active[c] = 0;
-        if (!isfinite(rn)) a.cs.status[c] = 1;
-      }
-    }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int cnt = 0;
-    for (int c = 0; c < KB; ++c) cnt += a.cs.active[c] != 0;
-    *a.cs.n_active = cnt;
   }
 }
 
@@ -721,6 +851,7 @@ __global__ __launch_bounds__(kBlock) void k_fin_rhs(FinArgs a) {
   __shared__ DDv s_out[KB];
   if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, KB, a.tree, s_in, s_out))
     return;
+  if (threadIdx.x == 0) *a.cs.upd_pending = 0;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     const double rr = dd_value(s_out[c]);
     a.cs.rho[c] = rr;
@@ -1044,41 +1175,50 @@ hipError_t launch_fill_f64(double* p, double v, int64_t count, hipStream_t s) {
 }
 
 template <int KB>
-static hipError_t fin_launch(int which, const FinArgs& f, hipStream_t s) {
-  const int grid = (f.nparts + kTreeFan - 1) / kTreeFan;
-  if (which == 0)
-    ERC_LAUNCH((k_fin_rhs<KB>), grid, s, f);
-  else if (which == 1)
-    ERC_LAUNCH((k_fin_spmm<KB>), grid, s, f);
-  else
-    ERC_LAUNCH((k_fin_update<KB>), grid, s, f);
+static hipError_t fin_rhs_launch(const FinArgs& f, hipStream_t s) {
+  ERC_LAUNCH((k_fin_rhs<KB>), (f.nparts + kTreeFan - 1) / kTreeFan, s, f);
   return hipGetLastError();
 }
 
-static hipError_t fin_dispatch(int which, int kb, const FinArgs& f, hipStream_t s) {
+template <int KB>
+static hipError_t fin_iter_launch(const IterArgs& f, hipStream_t s) {
+  const int np = f.nparts_s > f.nparts_u ? f.nparts_s : f.nparts_u;
+  ERC_LAUNCH((k_fin_iter<KB>), (np + kTreeFan - 1) / kTreeFan, s, f);
+  return hipGetLastError();
+}
+
+static hipError_t fin_rhs_dispatch(int kb, const FinArgs& f, hipStream_t s) {
   switch (kb) {
-    case 8: return fin_launch<8>(which, f, s);
-    case 16: return fin_launch<16>(which, f, s);
-    case 32: return fin_launch<32>(which, f, s);
-    case 64: return fin_launch<64>(which, f, s);
-    case 128: return fin_launch<128>(which, f, s);
-    case 256: return fin_launch<256>(which, f, s);
+    case 8: return fin_rhs_launch<8>(f, s);
+    case 16: return fin_rhs_launch<16>(f, s);
+    case 32: return fin_rhs_launch<32>(f, s);
+    case 64: return fin_rhs_launch<64>(f, s);
+    case 128: return fin_rhs_launch<128>(f, s);
+    case 256: return fin_rhs_launch<256>(f, s);
   }
   return hipErrorInvalidValue;
 }
 
-static FinArgs fin_args(const Work& w, int nparts) {
-  FinArgs f;
-  f.part = w.part;
-  f.nparts = nparts;
+hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream_t s) {
+  IterArgs f;
+  f.part_s = w.part;
+  f.nparts_s = g.grid;
+  f.part_u = w.part_u;
+  f.nparts_u = w.grid_upd;
   f.tree = w.tree;
   f.cs = w.cs;
   f.mega_dots = w.mega_dots;
-  f.nmega = 0;
-  f.gate = w.cs.n_active;
-  f.tol2 = 0.0;
-  f.ncols = 0;
-  return f;
+  f.nmega = g.nmega;
+  f.mode = mode;
+  switch (w.kb) {
+    case 8: return fin_iter_launch<8>(f, s);
+    case 16: return fin_iter_launch<16>(f, s);
+    case 32: return fin_iter_launch<32>(f, s);
+    case 64: return fin_iter_launch<64>(f, s);
+    case 128: return fin_iter_launch<128>(f, s);
+    case 256: return fin_iter_launch<256>(f, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <typename T, int KB>
@@ -1123,10 +1263,14 @@ hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int
   a.part = w.part;
   hipError_t e = rhs_dispatch(dt, w.kb, a, w.grid_rhs, s);
   if (e != hipSuccess) return e;
-  FinArgs f = fin_args(w, w.grid_rhs);
+  FinArgs f;
+  f.part = w.part;
+  f.nparts = w.grid_rhs;
+  f.tree = w.tree;
+  f.cs = w.cs;
   f.tol2 = tol * tol;
   f.ncols = ncols;
-  return fin_dispatch(0, w.kb, f, s);
+  return fin_rhs_dispatch(w.kb, f, s);
 }
 
 template <typename T, int LPN>
@@ -1152,28 +1296,24 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
   a.gate = gate;
   a.delta = delta;
   const int lpn = (dt == ERC_F32) ? w.kb / 4 : w.kb / 2;
-  hipError_t e = hipErrorInvalidValue;
   if (dt == ERC_F32) {
     switch (lpn) {
-      case 4: e = spmm_launch<float, 4>(a, s); break;
-      case 8: e = spmm_launch<float, 8>(a, s); break;
-      case 16: e = spmm_launch<float, 16>(a, s); break;
-      case 32: e = spmm_launch<float, 32>(a, s); break;
-      case 64: e = spmm_launch<float, 64>(a, s); break;
+      case 4: return spmm_launch<float, 4>(a, s);
+      case 8: return spmm_launch<float, 8>(a, s);
+      case 16: return spmm_launch<float, 16>(a, s);
+      case 32: return spmm_launch<float, 32>(a, s);
+      case 64: return spmm_launch<float, 64>(a, s);
     }
   } else {
     switch (lpn) {
-      case 4: e = spmm_launch<double, 4>(a, s); break;
-      case 8: e = spmm_launch<double, 8>(a, s); break;
-      case 16: e = spmm_launch<double, 16>(a, s); break;
-      case 32: e = spmm_launch<double, 32>(a, s); break;
-      case 64: e = spmm_launch<double, 64>(a, s); break;
+      case 4: return spmm_launch<double, 4>(a, s);
+      case 8: return spmm_launch<double, 8>(a, s);
+      case 16: return spmm_launch<double, 16>(a, s);
+      case 32: return spmm_launch<double, 32>(a, s);
+      case 64: return spmm_launch<double, 64>(a, s);
     }
   }
-  if (e != hipSuccess || gate != w.cs.n_active) return e;  // debug launches stop here
-  FinArgs f = fin_args(w, g.grid);
-  f.nmega = g.nmega;
-  return fin_dispatch(1, w.kb, f, s);
+  return hipErrorInvalidValue;
 }
 
 template <typename T, int CG>
@@ -1190,7 +1330,7 @@ hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStre
   a.q = w.q;
   const int vec = (dt == ERC_F32) ? 4 : 2;
   a.nvec = static_cast<int64_t>(g.n) * w.kb / vec;
-  a.part = w.part;
+  a.part = w.part_u;
   a.cs = w.cs;
   const int cg = w.kb / vec;
   const int grid = w.grid_upd;
@@ -1212,8 +1352,7 @@ hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStre
       case 64: e = upd_launch<double, 64>(a, grid, s); break;
     }
   }
-  if (e != hipSuccess) return e;
-  return fin_dispatch(2, w.kb, fin_args(w, grid), s);
+  return e;
 }
 
 template <typename T, int LPN>

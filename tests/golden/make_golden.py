@@ -1,0 +1,127 @@
+"""Write the stored oracle values used by the large-workload parity tests.
+
+    python tests/golden/make_golden.py cl170k [cl230k cl2400k ...]
+
+Each run regenerates the seeded graph, runs the CPU oracle (column-parallel, see
+oracle/parallel.py) over the workload's full projection, or over the column range
+named in RANGES, then computes curvature and sampling probabilities from that R and
+stores the values at seeded samples of edges and nodes in tests/golden/<name>.npz.
+Only gen/ and oracle/ are used; nothing here touches the GPU library.  The full oracle
+R is cached under $TMPDIR so the stored fields can be recomputed without the solve.
+
+Besides the values, each file stores, per sampled entry, the first-order error bound
+that a relative error `RTOL` in every edge curvature (measured on the condition scale
+2 (s_u + s_v) / R + |kappa|, s_u = 1/2 sum_v w_uv R_uv) induces in the sampling
+probabilities of Eqs. 7-8 and their normalisation:
+  node:  b_u = RTOL [sum_v (S_uv + S_x) + 2 q_u S_x] / D,  |dP_u| <= (b_u + P_u sum b) / Q
+  edge:  a_e = RTOL (2 S_x + S_e),  b_e = sqrt(x_e + a_e) - sqrt(max(x_e - a_e, 0)),
+         |dP_e| <= (b_e + P_e sum b) / Q_e
+with S the kappa scale, S_x the larger scale of the two extreme edges, D = kappa_max -
+kappa_min + eta and x_e = 2 kappa_max - kappa_e.
+"""
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+sys.path.insert(0, ROOT)
+
+import gen  # noqa: E402
+from oracle import erc as OE  # noqa: E402
+from oracle import graph as OG  # noqa: E402
+from oracle.parallel import resistance_parallel  # noqa: E402
+
+# column ranges for workloads whose full sketch is too long for the CPU oracle
+RANGES = {"cl2400k": (0, 64)}
+SAMPLES = 8192
+RTOL = 1e-4
+ORACLE_VERSION = 2  # bump when the oracle's arithmetic changes
+
+
+def log(msg):
+    print(f"[golden] {msg}", flush=True)
+
+
+def cache_path(name):
+    d = os.path.join(os.environ.get("TMPDIR", "/tmp"), "erc_golden_cache")
+    os.makedirs(d, exist_ok=True)
+    return os.path.join(d, f"{name}_R_v{ORACLE_VERSION}.npz")
+
+
+def sampling_bounds(g, R, kappa, s, node_prob, edge_prob, eta):
+    eu, ev, eid = OG.canonical_edges(g)
+    rows = OG.entry_rows(g)
+    S = 2.0 * (s[eu] + s[ev]) / R + np.abs(kappa)
+    kmin, kmax = float(kappa.min()), float(kappa.max())
+    Sx = max(S[np.argmin(kappa)], S[np.argmax(kappa)])
+    D = kmax - kmin + eta
+    qn = np.bincount(rows, weights=(kappa[eid] - kmin) / D, minlength=g.n)
+    bn = RTOL * (np.bincount(rows, weights=S[eid] + Sx, minlength=g.n) + 2.0 * qn * Sx) / D
+    Q = qn.sum()
+    bound_node = (bn + node_prob * bn.sum()) / Q
+    x = 2.0 * kmax - kappa
+    a = RTOL * (2.0 * Sx + S)
+    be = np.sqrt(x + a) - np.sqrt(np.maximum(x - a, 0.0))
+    qe = np.sqrt(np.maximum(x, 0.0)) + 1.0
+    bound_edge = (be + edge_prob * be.sum()) / qe.sum()
+    return S, bound_node, bound_edge, kmin, kmax
+
+
+def make(name, procs):
+    wl = gen.CONFIGS[name]
+    p = wl.params
+    t0 = time.time()
+    g = gen.make_graph(name, progress=log)
+    log(f"{name}: graph {g.summary()} ({time.time() - t0:.0f}s)")
+    c0, c1 = RANGES.get(name, (0, p.K))
+    cp = cache_path(name)
+    if os.path.exists(cp):
+        with np.load(cp) as f:
+            R, iters, conv, t_solve = f["R"], f["iters"], f["conv"], float(f["t_solve"])
+        log(f"{name}: oracle R from cache {cp}")
+    else:
+        t0 = time.time()
+        R, iters, conv = resistance_parallel(g, p.K, p.k_block, p.delta, p.tol, p.max_iter,
+                                             p.seed, p.dtype, c0, c1, procs=procs, progress=log)
+        t_solve = time.time() - t0
+        np.savez(cp, R=R, iters=iters, conv=conv, t_solve=t_solve)
+    log(f"{name}: resistance over columns [{c0}, {c1}) in {t_solve:.0f}s, "
+        f"iters {iters.min()}..{iters.max()}, all converged {bool(conv.all())}")
+    pn_p, kappa = OE.curvature(g, R)
+    node_prob, edge_prob = OE.sampling_probs(g, kappa, p.eta)
+    eu, ev, eid = OG.canonical_edges(g)
+    rows = OG.entry_rows(g)
+    w = np.ones(g.nnz) if g.w is None else np.asarray(g.w, np.float64)
+    s = 0.5 * np.bincount(rows, weights=w * R[eid], minlength=g.n)
+    S, bound_node, bound_edge, kmin, kmax = sampling_bounds(g, R, kappa, s, node_prob,
+                                                            edge_prob, p.eta)
+    rng = np.random.default_rng(12345)
+    es = np.sort(rng.choice(g.m, size=min(SAMPLES, g.m), replace=False))
+    ns = np.sort(rng.choice(g.n, size=min(SAMPLES, g.n), replace=False))
+    # the extreme-curvature edges are always in the sample
+    es = np.unique(np.concatenate([es, [np.argmin(kappa), np.argmax(kappa)]]))
+    meta = {"workload": name, "graph": g.summary(), "col_begin": c0, "col_end": c1,
+            "K": p.K, "k_block": p.k_block, "delta": p.delta, "tol": p.tol, "seed": p.seed,
+            "dtype": p.dtype, "eta": p.eta, "oracle_version": ORACLE_VERSION, "rtol": RTOL,
+            "solve_seconds": round(t_solve, 1), "procs": procs,
+            "iters_min": int(iters.min()), "iters_max": int(iters.max()),
+            "iters_total": int(iters.sum()), "converged": bool(conv.all()),
+            "kappa_min": kmin, "kappa_max": kmax,
+            "components": OG.components(g)}
+    out = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"{name}.npz")
+    np.savez_compressed(
+        out, meta=np.array(json.dumps(meta)), edge_idx=es, node_idx=ns,
+        R=R[es], kappa=kappa[es], kappa_scale=S[es], edge_prob=edge_prob[es],
+        edge_prob_bound=bound_edge[es], p=pn_p[ns], s_node=s[ns], node_prob=node_prob[ns],
+        node_prob_bound=bound_node[ns], iters=iters,
+        sum_wR=np.float64(np.sum(OG.edge_weights(g) * R)), sum_p=np.float64(pn_p.sum()))
+    log(f"wrote {out}")
+
+
+if __name__ == "__main__":
+    procs = int(os.environ.get("ERC_ORACLE_PROCS", "8"))
+    for name in sys.argv[1:]:
+        make(name, procs)
