@@ -1,11 +1,12 @@
-"""The five synthetic workloads and their solve parameters.
+"""The synthetic workloads and their solve parameters.
 
 Each workload is a seeded graph recipe shaped like one of the paper's evaluation
 graphs (Section 4: the SBM of Table 2, ogbn-arxiv, Reddit and ogbn-products of
 Table 3 and its text), plus the projection width K, the column block width, the
 diagonal shift delta (the paper's epsilon in Eq. 5), the CG tolerance tau, the
 working precision and the projection seed.  The datasets themselves are not used:
-these graphs stand in for them.
+these graphs stand in for them.  ORDER lists the five performance workloads; sbm2k is
+the smaller SBM of the curvature-agreement study (Table 2).
 """
 from __future__ import annotations
 
@@ -71,6 +72,13 @@ CONFIGS = {
         "chung_lu", {"n": 2_400_000, "gamma": 2.3, "i0": 398.2, "m_target": 62_000_000, "seed": 5,
                      "weighted": True, "keep_largest": False},
         SolveParams(K=256, k_block=64, delta=1e-4, tol=1e-5, dtype="f32", seed=105)),
+    "sbm2k": Workload(
+        "sbm2k",
+        "SBM, 10 blocks of 200, in-degree 10, cross-degree 1, U(0.5,2) weights; K up to "
+        "4096 in blocks of 64, fp32 (the curvature-agreement study of Table 2)",
+        "sbm", {"blocks": 10, "size": 200, "p_in": 10.0 / 199.0, "p_out": 1.0 / 1800.0,
+                "seed": 6},
+        SolveParams(K=4096, k_block=64, delta=1e-5, tol=1e-6, dtype="f32", seed=106)),
 }
 
 ORDER = ["er2k", "sbm20k", "cl170k", "cl230k", "cl2400k"]
