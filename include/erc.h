@@ -195,6 +195,44 @@ erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
                               void* scratch_dev, size_t scratch_bytes,
                               double* node_prob_dev, double* edge_prob_dev, void* stream);
 
+/* ---- curvature-guided subgraph draws (Section 3.2; Section 4) --------------------- */
+
+/* Which distribution a draw uses and what a subgraph is built from. */
+typedef enum { ERC_NODES = 0, ERC_EDGES = 1 } erc_items;
+
+/* Device scratch of erc_draw over the n nodes or the m edges. */
+erc_status erc_draw_scratch_bytes(erc_handle h, erc_items items, size_t* bytes);
+
+/* idx_dev[d] (device, draws int64), d = 0 .. draws-1: independent draws from the
+ * distribution prob_dev (device fp64, n entries for ERC_NODES, m for ERC_EDGES; each in
+ * [0, 1], summing to one up to rounding, as erc_sampling_probs writes them).
+ * Definition: W_i = floor(P_i 2^62), C_i = sum_{j<i} W_j, T = C_N (exact 64-bit
+ * integers); draw d takes X = x_hi 2^64 + x_lo with x_hi, x_lo the outputs 2d and 2d+1
+ * of SplitMix64 started from the first output of SplitMix64(seed), t = floor(X T / 2^128),
+ * and returns the i with C_i <= t < C_{i+1}.  Items with W_i = 0 are never drawn.
+ * scratch_dev: >= erc_draw_scratch_bytes bytes.  Blocks until the stream has drained.
+ * ERC_E_NUMERIC (idx_dev filled with -1) when a probability is NaN or outside [0, 1],
+ * when they sum above 1.5, or when every W_i is 0. */
+erc_status erc_draw(erc_handle h, erc_items items, const double* prob_dev, int64_t draws,
+                    uint64_t seed, void* scratch_dev, size_t scratch_bytes, int64_t* idx_dev,
+                    void* stream);
+
+/* Device scratch of erc_subgraph. */
+erc_status erc_subgraph_scratch_bytes(erc_handle h, size_t* bytes);
+
+/* Training subgraph from count drawn indices idx_dev (device int64; repeats allowed).
+ * ERC_NODES: the subgraph induced on the distinct drawn nodes.  ERC_EDGES: the distinct
+ * drawn edges and their endpoints.  Outputs (device): nodes_dev (int32, capacity n) the
+ * kept nodes in increasing id, which renumbers them 0..n_s-1; edges_dev (int64,
+ * capacity m) the kept canonical edge ids in increasing order; u_dev, v_dev (int32,
+ * capacity m) each kept edge's endpoints u < v in the new numbering.  counts_host[0] =
+ * n_s, counts_host[1] = m_s (host).  Blocks until the stream has drained.
+ * ERC_E_INVALID_ARG when an index is outside [0, n) or [0, m) (outputs undefined). */
+erc_status erc_subgraph(erc_handle h, erc_items items, const int64_t* idx_dev, int64_t count,
+                        void* scratch_dev, size_t scratch_bytes, int32_t* nodes_dev,
+                        int64_t* edges_dev, int32_t* u_dev, int32_t* v_dev,
+                        int64_t* counts_host, void* stream);
+
 /* ---- diagnostics ----------------------------------------------------------------- */
 
 const char* erc_status_string(erc_status s);

@@ -58,6 +58,14 @@ def _desc(rowptr, col, w, solve_dtype):
     return d, keep
 
 
+def _items(items) -> int:
+    if items in ("nodes", _abi.ERC_NODES):
+        return _abi.ERC_NODES
+    if items in ("edges", _abi.ERC_EDGES):
+        return _abi.ERC_EDGES
+    raise ValueError(f"items must be 'nodes' or 'edges', not {items!r}")
+
+
 def validate(rowptr, col, w=None, solve_dtype="f32") -> int:
     """Host-only check of a CSR graph; returns the number of undirected edges."""
     d, _keep = _desc(rowptr, col, w, solve_dtype)
@@ -86,6 +94,7 @@ class Graph:
         self.nnz = int(np.asarray(rowptr)[-1])
         self._ws = {}
         self._scratch = None
+        self._scratches = {}
 
     def _stream(self) -> int:
         return self.torch.cuda.current_stream(self.device).cuda_stream
@@ -149,6 +158,44 @@ class Graph:
         _abi.erc_sampling_probs(self.handle, kappa.data_ptr(), eta, self._scratch.data_ptr(),
                                 self._scratch.numel(), pn.data_ptr(), pe.data_ptr(), self._stream())
         return pn, pe[: self.m]
+
+    def _scratch_of(self, key, nbytes):
+        buf = self._scratches.get(key)
+        if buf is None or buf.numel() < nbytes:
+            buf = self.torch.empty(max(nbytes, 256), dtype=self.torch.uint8, device=self.device)
+            self._scratches[key] = buf
+        return buf
+
+    def draw(self, items, prob, draws, seed):
+        """`draws` indices (torch int64) drawn from the node ("nodes") or edge ("edges")
+        distribution `prob` (device fp64, as sampling_probs returns it)."""
+        it = _items(items)
+        prob = prob.to(self.device, self.torch.float64).contiguous()
+        need = self.n if it == _abi.ERC_NODES else self.m
+        if prob.numel() != need:
+            raise ValueError(f"prob has {prob.numel()} entries, expected {need}")
+        sc = self._scratch_of(("draw", it), _abi.erc_draw_scratch_bytes(self.handle, it))
+        idx = self.torch.empty(max(draws, 1), dtype=self.torch.int64, device=self.device)
+        _abi.erc_draw(self.handle, it, prob.data_ptr(), draws, seed, sc.data_ptr(), sc.numel(),
+                      idx.data_ptr(), self._stream())
+        return idx[:draws]
+
+    def subgraph(self, items, idx):
+        """Subgraph from drawn indices: induced on the drawn nodes ("nodes"), or the drawn
+        edges and their endpoints ("edges").  Returns the kept node ids, the kept edge ids
+        and the kept edges' endpoints renumbered to positions in the node list."""
+        torch = self.torch
+        it = _items(items)
+        idx = idx.to(self.device, torch.int64).contiguous()
+        sc = self._scratch_of("subgraph", _abi.erc_subgraph_scratch_bytes(self.handle))
+        nodes = torch.empty(max(self.n, 1), dtype=torch.int32, device=self.device)
+        edges = torch.empty(max(self.m, 1), dtype=torch.int64, device=self.device)
+        u = torch.empty(max(self.m, 1), dtype=torch.int32, device=self.device)
+        v = torch.empty(max(self.m, 1), dtype=torch.int32, device=self.device)
+        ns, ms = _abi.erc_subgraph(self.handle, it, idx.data_ptr(), idx.numel(), sc.data_ptr(),
+                                   sc.numel(), nodes.data_ptr(), edges.data_ptr(), u.data_ptr(),
+                                   v.data_ptr(), self._stream())
+        return {"nodes": nodes[:ns], "edges": edges[:ms], "u": u[:ms], "v": v[:ms]}
 
     def edge_endpoints(self):
         torch = self.torch

@@ -24,6 +24,8 @@ ERC_E_STATE = 7
 
 ERC_F32 = 0
 ERC_F64 = 1
+ERC_NODES = 0
+ERC_EDGES = 1
 ERC_ACCUMULATE = 1
 ERC_PROFILE_SPMM = 2
 
@@ -86,6 +88,12 @@ _SIGNATURES = {
     "erc_sampling_scratch_bytes": [c_void_p, POINTER(c_size_t)],
     "erc_sampling_probs": [c_void_p, c_void_p, c_double, c_void_p, c_size_t, c_void_p, c_void_p,
                            c_void_p],
+    "erc_draw_scratch_bytes": [c_void_p, c_int, POINTER(c_size_t)],
+    "erc_draw": [c_void_p, c_int, c_void_p, c_int64, c_uint64, c_void_p, c_size_t, c_void_p,
+                 c_void_p],
+    "erc_subgraph_scratch_bytes": [c_void_p, POINTER(c_size_t)],
+    "erc_subgraph": [c_void_p, c_int, c_void_p, c_int64, c_void_p, c_size_t, c_void_p, c_void_p,
+                     c_void_p, c_void_p, POINTER(c_int64), c_void_p],
     "erc_status_string": [c_int],
     "erc_last_error": [],
     "erc_debug_check_plan": [POINTER(erc_graph_desc)],
@@ -203,6 +211,33 @@ def erc_sampling_probs(h: int, kappa_dev: int, eta: float, scratch: int, scratch
     _check(load().erc_sampling_probs(c_void_p(h), c_void_p(kappa_dev), eta, c_void_p(scratch),
                                      scratch_bytes, c_void_p(pn_dev), c_void_p(pe_dev),
                                      c_void_p(stream)))
+
+
+def erc_draw_scratch_bytes(h: int, items: int) -> int:
+    b = c_size_t(0)
+    _check(load().erc_draw_scratch_bytes(c_void_p(h), items, byref(b)))
+    return b.value
+
+
+def erc_draw(h: int, items: int, prob_dev: int, draws: int, seed: int, scratch: int,
+             scratch_bytes: int, idx_dev: int, stream: int) -> None:
+    _check(load().erc_draw(c_void_p(h), items, c_void_p(prob_dev), draws, seed,
+                           c_void_p(scratch), scratch_bytes, c_void_p(idx_dev), c_void_p(stream)))
+
+
+def erc_subgraph_scratch_bytes(h: int) -> int:
+    b = c_size_t(0)
+    _check(load().erc_subgraph_scratch_bytes(c_void_p(h), byref(b)))
+    return b.value
+
+
+def erc_subgraph(h: int, items: int, idx_dev: int, count: int, scratch: int, scratch_bytes: int,
+                 nodes_dev: int, edges_dev: int, u_dev: int, v_dev: int, stream: int):
+    counts = (c_int64 * 2)()
+    _check(load().erc_subgraph(c_void_p(h), items, c_void_p(idx_dev), count, c_void_p(scratch),
+                               scratch_bytes, c_void_p(nodes_dev), c_void_p(edges_dev),
+                               c_void_p(u_dev), c_void_p(v_dev), counts, c_void_p(stream)))
+    return int(counts[0]), int(counts[1])
 
 
 def erc_status_string(status: int) -> str:

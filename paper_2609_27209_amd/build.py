@@ -2,8 +2,8 @@
 
     python -m paper_2609_27209_amd.build
 
-Compiles ``csrc/erc_kernels.hip`` and ``csrc/erc_host.cpp`` with hipcc and links them
-into ``paper_2609_27209_amd/liberc.so``.  Packed fp32 instructions are disabled in
+Compiles ``csrc/erc_kernels.hip``, ``csrc/erc_draw.hip`` and ``csrc/erc_host.cpp`` with
+hipcc and links them into ``paper_2609_27209_amd/liberc.so``.  Packed fp32 instructions are disabled in
 device code (``-packed-fp32-ops``); the host pass warns that it does not know the
 feature, which is harmless.
 """
@@ -47,18 +47,19 @@ def build(verbose: bool = False) -> str:
     hipcc = _hipcc()
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
-    kern_o = os.path.join(objdir, "erc_kernels.o")
-    host_o = os.path.join(objdir, "erc_host.o")
-    jobs = [
-        [hipcc, f"--offload-arch={ARCH}", *COMMON, *DEVICE, "-c",
-         os.path.join(CSRC, "erc_kernels.hip"), "-o", kern_o],
-        [hipcc, *COMMON, "-c", os.path.join(CSRC, "erc_host.cpp"), "-o", host_o],
-    ]
-    with ThreadPoolExecutor(2) as ex:
+    objs = []
+    jobs = []
+    for name in ("erc_kernels", "erc_draw"):
+        objs.append(os.path.join(objdir, name + ".o"))
+        jobs.append([hipcc, f"--offload-arch={ARCH}", *COMMON, *DEVICE, "-c",
+                     os.path.join(CSRC, name + ".hip"), "-o", objs[-1]])
+    objs.append(os.path.join(objdir, "erc_host.o"))
+    jobs.append([hipcc, *COMMON, "-c", os.path.join(CSRC, "erc_host.cpp"), "-o", objs[-1]])
+    with ThreadPoolExecutor(len(jobs)) as ex:
         for f in [ex.submit(_run, j, verbose) for j in jobs]:
             f.result()
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, host_o, "-o", tmp], verbose)
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 

@@ -32,6 +32,7 @@ struct DevGraph {
   const void* w;             // nnz, working precision
   const int32_t* eid;        // nnz, canonical edge id of each entry
   const double* sw;          // m, sqrt(w_e) rounded once from fp64(w_e)
+  int sw_from_w;             // 1 if w holds the input weights exactly (sqrt on the fly)
   const int64_t* ubase;      // n+1, id of the first edge (u, v>u) of row u
 
   // SpMM plan: per-wave ranges over `light`, plus block-cooperative tasks for long rows
@@ -132,5 +133,32 @@ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t tree_ticks(int grid) {
   return ceil_div(grid, kTreeFan) + ceil_div(grid, kTreeFan * kTreeFan) + 1;
 }
+
+// Subgraph draws (erc_draw.hip).  Status bits a launch leaves in its status word.
+constexpr uint32_t kDrawBadProb = 1u;      // a probability outside [0, 1] or NaN
+constexpr uint32_t kDrawSumTooLarge = 2u;  // probabilities sum above 1.5
+constexpr uint32_t kDrawAllZero = 4u;      // every integer weight is zero
+constexpr uint32_t kSubBadIndex = 8u;      // a drawn index outside the node or edge range
+constexpr int64_t kScanTile = 4096;        // items per block of the prefix-sum kernels
+inline int64_t scan_blocks(int64_t items) { return ceil_div(items, kScanTile); }
+
+struct DrawWork {
+  uint64_t* cdf;     // N+1: exclusive prefix sums of the integer weights, cdf[N] = total
+  uint64_t* bsum;    // scan_blocks(N) block sums
+  double* psum;      // scan_blocks(N) fp64 block sums of the probabilities
+  uint32_t* status;  // one word, zero before the launch
+};
+struct SubgraphWork {
+  uint32_t* npos;    // n+1: node flags, then their exclusive prefix sums (new ids)
+  uint32_t* epos;    // m+1: edge flags, then their exclusive prefix sums
+  uint32_t* bsum;    // scan_blocks(max(n, m)) block sums
+  uint32_t* status;  // one word, zero before the launch
+};
+hipError_t launch_draw(const double* prob, int64_t N, int64_t draws, uint64_t base,
+                       const DrawWork& w, int64_t* idx, hipStream_t s);
+// items 0: subgraph induced on the nodes in idx; 1: the edges in idx and their endpoints
+hipError_t launch_subgraph(const DevGraph& g, int items, const int64_t* idx, int64_t count,
+                           const SubgraphWork& w, int32_t* nodes, int64_t* edges, int32_t* uo,
+                           int32_t* vo, hipStream_t s);
 
 }  // namespace erc

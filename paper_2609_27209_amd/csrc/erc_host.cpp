@@ -726,6 +726,8 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   g.nnz = nnz;
   g.m = c.m;
   g.weighted = weighted ? 1 : 0;
+  // the stored weights equal the input ones unless fp64 input is rounded to fp32
+  g.sw_from_w = (weighted && !(desc->w_dtype == ERC_F64 && desc->solve_dtype == ERC_F32)) ? 1 : 0;
   g.rowptr = reinterpret_cast<const int64_t*>(base + L.rowptr);
   g.col = reinterpret_cast<const int32_t*>(base + L.col);
   g.w = weighted ? base + L.w : nullptr;
@@ -942,6 +944,139 @@ erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
   ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
   ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
   ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
+  return ERC_OK;
+}
+
+namespace {
+struct DrawLayout {
+  int64_t cdf, bsum, psum, status, total;
+};
+DrawLayout draw_layout(int64_t N) {
+  DrawLayout L{};
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off = align_up(off + std::max<int64_t>(bytes, 0), 256);
+    return at;
+  };
+  const int64_t nb = std::max<int64_t>(1, scan_blocks(N));
+  L.cdf = take((N + 1) * 8);
+  L.bsum = take(nb * 8);
+  L.psum = take(nb * 8);
+  L.status = take(4);
+  L.total = off;
+  return L;
+}
+struct SubLayout {
+  int64_t npos, epos, bsum, status, total;
+};
+SubLayout sub_layout(const erc_graph_s* h) {
+  SubLayout L{};
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off = align_up(off + std::max<int64_t>(bytes, 0), 256);
+    return at;
+  };
+  L.npos = take((h->n + 1) * 4);
+  L.epos = take((h->m + 1) * 4);
+  L.bsum = take(std::max<int64_t>(1, scan_blocks(std::max(h->n, h->m))) * 4);
+  L.status = take(4);
+  L.total = off;
+  return L;
+}
+erc_status read_status(uint32_t* status_dev, hipStream_t s, uint32_t* out) {
+  ERC_HIP(hipMemcpyAsync(out, status_dev, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipStreamSynchronize(s));
+  return ERC_OK;
+}
+}  // namespace
+
+erc_status erc_draw_scratch_bytes(erc_handle h, erc_items items, size_t* bytes) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+  *bytes = static_cast<size_t>(draw_layout(items == ERC_NODES ? h->n : h->m).total);
+  return ERC_OK;
+}
+
+erc_status erc_draw(erc_handle h, erc_items items, const double* prob_dev, int64_t draws,
+                    uint64_t seed, void* scratch_dev, size_t scratch_bytes, int64_t* idx_dev,
+                    void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+  const int64_t N = items == ERC_NODES ? h->n : h->m;
+  if (N <= 0) return fail(ERC_E_INVALID_ARG, "no items to draw from");
+  if (draws < 0) return fail(ERC_E_INVALID_ARG, "draws must be >= 0");
+  if (prob_dev == nullptr || scratch_dev == nullptr || (draws > 0 && idx_dev == nullptr))
+    return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const DrawLayout L = draw_layout(N);
+  if (static_cast<int64_t>(scratch_bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_draw_scratch_bytes");
+  char* b = static_cast<char*>(scratch_dev);
+  DrawWork w{};
+  w.cdf = reinterpret_cast<uint64_t*>(b + L.cdf);
+  w.bsum = reinterpret_cast<uint64_t*>(b + L.bsum);
+  w.psum = reinterpret_cast<double*>(b + L.psum);
+  w.status = reinterpret_cast<uint32_t*>(b + L.status);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
+  ERC_HIP(launch_draw(prob_dev, N, draws, splitmix_first(seed), w, idx_dev, s));
+  uint32_t st = 0;
+  erc_status rs = read_status(w.status, s, &st);
+  if (rs != ERC_OK) return rs;
+  if (st & kDrawBadProb) return fail(ERC_E_NUMERIC, "a probability is NaN or outside [0, 1]");
+  if (st & kDrawSumTooLarge) return fail(ERC_E_NUMERIC, "probabilities sum above 1.5");
+  if (st & kDrawAllZero) return fail(ERC_E_NUMERIC, "every probability rounds to a zero weight");
+  return ERC_OK;
+}
+
+erc_status erc_subgraph_scratch_bytes(erc_handle h, size_t* bytes) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+  *bytes = static_cast<size_t>(sub_layout(h).total);
+  return ERC_OK;
+}
+
+erc_status erc_subgraph(erc_handle h, erc_items items, const int64_t* idx_dev, int64_t count,
+                        void* scratch_dev, size_t scratch_bytes, int32_t* nodes_dev,
+                        int64_t* edges_dev, int32_t* u_dev, int32_t* v_dev,
+                        int64_t* counts_host, void* stream) {
+  g_last_error.clear();
+  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+  if (count < 0) return fail(ERC_E_INVALID_ARG, "count must be >= 0");
+  if (scratch_dev == nullptr || counts_host == nullptr || nodes_dev == nullptr ||
+      (count > 0 && idx_dev == nullptr) ||
+      (h->m > 0 && (edges_dev == nullptr || u_dev == nullptr || v_dev == nullptr)))
+    return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  if (items == ERC_EDGES && h->m == 0 && count > 0)
+    return fail(ERC_E_INVALID_ARG, "the graph has no edges");
+  const SubLayout L = sub_layout(h);
+  if (static_cast<int64_t>(scratch_bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_subgraph_scratch_bytes");
+  char* b = static_cast<char*>(scratch_dev);
+  SubgraphWork w{};
+  w.npos = reinterpret_cast<uint32_t*>(b + L.npos);
+  w.epos = reinterpret_cast<uint32_t*>(b + L.epos);
+  w.bsum = reinterpret_cast<uint32_t*>(b + L.bsum);
+  w.status = reinterpret_cast<uint32_t*>(b + L.status);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
+  ERC_HIP(launch_subgraph(h->dg, items == ERC_NODES ? 0 : 1, idx_dev, count, w, nodes_dev,
+                          edges_dev, u_dev, v_dev, s));
+  uint32_t tot[2] = {0u, 0u};
+  ERC_HIP(hipMemcpyAsync(&tot[0], w.npos + h->n, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(&tot[1], w.epos + h->m, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+  uint32_t st = 0;
+  erc_status rs = read_status(w.status, s, &st);
+  if (rs != ERC_OK) return rs;
+  if (st & kSubBadIndex) return fail(ERC_E_INVALID_ARG, "a drawn index is out of range");
+  counts_host[0] = tot[0];
+  counts_host[1] = tot[1];
   return ERC_OK;
 }
 

@@ -274,7 +274,10 @@ __device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
 // columns [sub*VEC, sub*VEC + VEC).  Each lane issues kInflight row loads before it
 // consumes them, so a wavefront keeps kInflight * 1 KB of gathers in flight.  Slots past
 // the end read p_i with weight 0, which adds exactly zero.
-constexpr int kInflight = 4;
+#ifndef ERC_SPMM_INFLIGHT
+#define ERC_SPMM_INFLIGHT 8
+#endif
+constexpr int kInflight = ERC_SPMM_INFLIGHT;
 
 template <typename T, int LPN, bool W>
 __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
@@ -687,6 +690,11 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
   }
 }
 
+#ifndef ERC_UPD_UNROLL
+#define ERC_UPD_UNROLL 2
+#endif
+constexpr int kUpdUnroll = ERC_UPD_UNROLL;
+
 struct UpdArgs {
   void* z;
   void* r;
@@ -722,21 +730,39 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
   T* __restrict__ R = static_cast<T*>(a.r);
   T* __restrict__ P = static_cast<T*>(a.p);
   const T* __restrict__ Qv = static_cast<const T*>(a.q);
+  // kUpdUnroll vectors per thread per step, loads of all of them issued first
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-  for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < a.nvec; x += stride) {
-    const int64_t o = x * VEC;
-    V<T> z = ldv_nt(Z + o), r = ldv_nt(R + o), p = ldv_nt(P + o);
-    const V<T> q = ldv_nt(Qv + o);
+  for (int64_t x0 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x0 < a.nvec;
+       x0 += stride * kUpdUnroll) {
+    V<T> z[kUpdUnroll], r[kUpdUnroll], p[kUpdUnroll], q[kUpdUnroll];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) {
-      z.x[v] += al[v] * p.x[v];
-      r.x[v] -= al[v] * q.x[v];
-      if (act[v]) p.x[v] = r.x[v] + be[v] * p.x[v];
-      part[v].add(r.x[v], r.x[v]);
+    for (int u = 0; u < kUpdUnroll; ++u) {
+      const int64_t x = x0 + u * stride;
+      if (x < a.nvec) {
+        const int64_t o = x * VEC;
+        z[u] = ldv_nt(Z + o);
+        r[u] = ldv_nt(R + o);
+        p[u] = ldv_nt(P + o);
+        q[u] = ldv_nt(Qv + o);
+      }
     }
-    stv_nt(Z + o, z);
-    stv_nt(R + o, r);
-    stv(P + o, p);  // p is gathered by the next SpMM
+#pragma unroll
+    for (int u = 0; u < kUpdUnroll; ++u) {
+      const int64_t x = x0 + u * stride;
+      if (x < a.nvec) {
+        const int64_t o = x * VEC;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+          z[u].x[v] += al[v] * p[u].x[v];
+          r[u].x[v] -= al[v] * q[u].x[v];
+          if (act[v]) p[u].x[v] = r[u].x[v] + be[v] * p[u].x[v];
+          part[v].add(r[u].x[v], r[u].x[v]);
+        }
+        stv_nt(Z + o, z[u]);
+        stv_nt(R + o, r[u]);
+        stv(P + o, p[u]);  // p is gathered by the next SpMM
+      }
+    }
   }
 #pragma unroll
   for (int v = 0; v < VEC; ++v) s_part[threadIdx.x][v] = part[v].get();
@@ -792,7 +818,15 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
       if (lane < cnt) {
         myj = a.g.col[base + lane];
         mye = a.g.eid[base + lane];
-        mysw = a.g.sw[mye];
+        // sqrt(w_e): from the entry's own weight when it holds the input value exactly
+        // (a correctly rounded fp64 sqrt, the same value the host stores per edge), else
+        // from the per-edge table
+        if (!a.g.weighted)
+          mysw = 1.0;
+        else if (a.g.sw_from_w)
+          mysw = sqrt(static_cast<double>(static_cast<const T*>(a.g.w)[base + lane]));
+        else
+          mysw = a.g.sw[mye];
       }
       for (int k = 0; k < cnt; ++k) {
         const int j = __builtin_amdgcn_readlane(myj, k);

@@ -1,0 +1,65 @@
+"""GPU: the curvature-agreement study of Table 2 with this path as ERC-LG.
+
+ERC-LG (CG on the GPU) and ERC-JL (same sketch, dense direct solve in the oracle)
+must give nearly identical curvatures and scores against the pseudoinverse
+reference at every K, and the error must fall with K at about the K^(-1/2) rate of
+the JL estimate."""
+import os
+
+import numpy as np
+import pytest
+
+import agreement_study as S
+from oracle import agreement as AG
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not os.path.exists(S.GOLDEN), reason="agreement goldens missing")]
+
+
+@pytest.fixture(scope="module")
+def result():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    meta, gold, rows, lg = S.study()
+    print("\n" + S.format_table(rows), flush=True)
+    return meta, gold, rows, lg
+
+
+def test_lg_matches_dense_jl_per_edge(result):
+    meta, gold, rows, lg = result
+    for K in meta["Ks"]:
+        R, kappa, info = lg[K]
+        assert info["cols_unconverged"] == 0
+        Rj = gold[f"R_jl_{K}"]
+        kj = gold[f"kappa_jl_{K}"]
+        # CG stops at a relative residual of tol per column: the resistances agree to a
+        # small multiple of it, the curvatures on their own scale (Eq. 2)
+        rel_R = np.abs(R - Rj) / Rj
+        assert rel_R.max() < 1e-3, (K, rel_R.max())
+        scale = np.abs(kj) + 2.0 / Rj
+        rel_k = np.abs(kappa - kj) / scale
+        assert rel_k.max() < 1e-3, (K, rel_k.max())
+
+
+def test_lg_and_jl_scores_nearly_identical(result):
+    meta, gold, rows, lg = result
+    by = {(r["K"], r["method"]): r for r in rows}
+    m = len(gold["kappa_pinv"])
+    for K in meta["Ks"]:
+        jl, cg = by[(K, "ERC-JL")], by[(K, "ERC-LG")]
+        assert abs(cg["mae"] - jl["mae"]) <= 1e-3 * jl["mae"]
+        assert abs(cg["spearman"] - jl["spearman"]) <= 1e-4
+        assert abs(cg["sign"] - jl["sign"]) <= 3.0 / m
+
+
+def test_agreement_improves_with_k(result):
+    meta, gold, rows, lg = result
+    lgrows = [r for r in rows if r["method"] == "ERC-LG"]
+    maes = [r["mae"] for r in lgrows]
+    assert maes[0] > maes[1] > maes[2]
+    assert 1.6 < maes[0] / maes[2] < 2.5   # K grows 4x: error ~ K^(-1/2) halves
+    assert lgrows[0]["spearman"] < lgrows[2]["spearman"]
+    assert lgrows[0]["sign"] < lgrows[2]["sign"]
+    reg = rows[0]
+    assert reg["mae"] < 1e-4 and reg["sign"] == 1.0
