@@ -8,6 +8,9 @@ before the timed region starts.  Prints ONE JSON line on stdout; progress goes t
 stderr.
 
     python bench.py [--steps K] [--warmup W] [--config cl2400k] [--no-cpu-baseline]
+
+After the timed steps it also times one curvature-guided training subgraph per
+distribution (erc_draw + erc_subgraph; not part of a step) unless --no-draw.
 """
 import argparse
 import json
@@ -29,8 +32,8 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 # the kernel source it was measured on: reported as null once that file changes.
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
-    "kernel_sha256_16": "4d967d41617a722b",
-    "fetch_bytes": 33616574706,
+    "kernel_sha256_16": "9006a9f6538a32e2",
+    "fetch_bytes": 33618020048,
     "write_bytes": 639565824,
     "profile": "profiles/k_spmm_cl2400k.md",
 }
@@ -63,7 +66,7 @@ def padded(kb: int, dtype: str) -> int:
     return w
 
 
-def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 50, cg_iters: int = 4):
+def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 25, cg_iters: int = 16):
     """Time the CPU oracle on a bounded sample of this workload and scale to edges/s.
 
     Sample: a 1/`scale_div` instance of the same graph recipe (n and m divided by
@@ -121,6 +124,32 @@ def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 50, cg_iters: int 
             "sample": sample, "est_seconds": round(total, 1)}
 
 
+def subgraph_draw(G, pn, pe, torch, reps: int = 5):
+    """Time one curvature-guided training subgraph per distribution, outside the timed
+    steps: erc_draw (1% of the nodes, or 0.1% of the edges, as draws) then erc_subgraph
+    on the probabilities of the last step, median over `reps` with HIP events."""
+    out = {}
+    for items, prob, draws in (("nodes", pn, max(1, G.n // 100)),
+                               ("edges", pe, max(1, G.m // 1000))):
+        ts, sizes = [], None
+        for r in range(reps + 1):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            idx = G.draw(items, prob, draws, seed=1000 + r)
+            sg = G.subgraph(items, idx)
+            e1.record()
+            torch.cuda.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1))
+            sizes = (sg["nodes"].numel(), sg["edges"].numel())
+        ts.sort()
+        out[items] = {"draws": draws, "ms": round(ts[len(ts) // 2], 3),
+                      "subgraph_nodes": sizes[0], "subgraph_edges": sizes[1]}
+        log(f"subgraph draw ({items}): {out[items]}")
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -128,8 +157,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="cl2400k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-scale", type=int, default=50,
+    ap.add_argument("--cpu-scale", type=int, default=25,
                     help="the CPU baseline runs on a 1/cpu-scale instance of the workload")
+    ap.add_argument("--no-draw", action="store_true",
+                    help="skip the subgraph-draw measurement after the timed steps")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this size 3 times (a plain "
                          "copy kernel of known size, to calibrate HBM byte counters)")
@@ -160,11 +191,14 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"erc_create {time.perf_counter() - t0:.1f}s")
 
+    last = {}
+
     def step(profile: bool):
         R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed,
                                profile=profile)
         pp, kk = G.curvature(R)
         pn, pe = G.sampling_probs(kk, p.eta)
+        last["pn"], last["pe"] = pn, pe
         return info
 
     for i in range(args.warmup):
@@ -209,6 +243,8 @@ def main() -> int:
         roofline["traffic_frac"] = round(tb / PEAK_HBM_GBS, 4)
     iters_total = infos[-1]["iters_total"]
 
+    draw = None if args.no_draw else subgraph_draw(G, last["pn"], last["pe"], torch)
+
     if args.copy_probe_mib > 0:
         nb = args.copy_probe_mib << 20
         src = torch.ones(nb // 4, dtype=torch.float32, device="cuda")
@@ -223,7 +259,10 @@ def main() -> int:
     if not args.no_cpu_baseline:
         try:
             t0 = time.perf_counter()
-            cpu = cpu_baseline(g, p, wl, iters_total, args.cpu_scale)
+            from threadpoolctl import threadpool_limits
+
+            with threadpool_limits(limits=1):  # the oracle runs on one host thread
+                cpu = cpu_baseline(g, p, wl, iters_total, args.cpu_scale)
             cpu["sample_wall_s"] = round(time.perf_counter() - t0, 1)
         except MemoryError as exc:  # pragma: no cover - host-dependent
             log(f"cpu baseline skipped: {exc}")
@@ -246,6 +285,7 @@ def main() -> int:
                    "seed": p.seed, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "subgraph_draw": draw,
         "solve": {"iters_max": infos[-1]["iters_max"], "iters_total": iters_total,
                   "max_final_relres": infos[-1]["max_final_relres"],
                   "ms_rhs": infos[-1]["ms_rhs"], "ms_cg": infos[-1]["ms_cg"],
