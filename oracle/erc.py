@@ -127,6 +127,62 @@ def cg_columns(L, delta: float, Y: np.ndarray, tol: float, max_iter: int) -> CGR
     return CGResult(Z, iters, ~active, relres)
 
 
+def jacobi_inverse(L, delta: float) -> np.ndarray:
+    """m_i = 1 / (L_ii + delta): the inverse diagonal of L + delta I, in fp64."""
+    return 1.0 / (np.asarray(L.diagonal(), dtype=np.float64) + delta)
+
+
+def pcg_columns(L, delta: float, Y: np.ndarray, tol: float, max_iter: int) -> CGResult:
+    """Jacobi-preconditioned CG for every column of (L + delta I) Z = Y.
+
+    A variant the paper does not use: textbook preconditioned CG (Saad, Iterative
+    Methods for Sparse Linear Systems, 2nd ed., Algorithm 9.1) with M^-1 = diag(m),
+    m_i = 1 / (L_ii + delta).  Per column c: z = 0, r = y, s = m * r, p = s,
+    rho = r.s.  Each iteration forms q = (L + delta I) p, alpha = rho / (p.q),
+    z += alpha p, r -= alpha q; the column stops once r.r <= tol^2 y.y (the stopping
+    test of plain CG), else s = m * r, rho' = r.s and p = s + (rho'/rho) p.  Inner
+    products in twice the working precision, as for plain CG.
+    """
+    Y = np.asarray(Y, dtype=np.float64)
+    n, k = Y.shape
+    m = jacobi_inverse(L, delta)[:, None]
+    Z = np.zeros((n, k))
+    R = Y.copy()
+    S = m * R
+    P = S.copy()
+    rho = dot2_columns(R, S)
+    rr0 = dot2_columns(R, R)
+    rr = rr0.copy()
+    thr = tol * tol * rr0
+    active = rr0 > 0
+    iters = np.zeros(k, dtype=np.int64)
+    for it in range(1, max_iter + 1):
+        a = np.flatnonzero(active)
+        if a.size == 0:
+            break
+        Pa = P[:, a]
+        Qa = laplacian_apply(L, delta, Pa)
+        pi = dot2_columns(Pa, Qa)
+        if np.any(~np.isfinite(pi)) or np.any(pi <= 0):
+            raise CGBreakdown(f"p.q <= 0 or non-finite at iteration {it}")
+        alpha = rho[a] / pi
+        Z[:, a] += alpha * Pa
+        Ra = R[:, a] - alpha * Qa
+        R[:, a] = Ra
+        rr[a] = dot2_columns(Ra, Ra)
+        iters[a] = it
+        done = rr[a] <= thr[a]
+        Sa = m * Ra
+        rho_new = dot2_columns(Ra, Sa)
+        beta = rho_new / rho[a]
+        keep = ~done
+        P[:, a[keep]] = Sa[:, keep] + beta[keep] * Pa[:, keep]
+        rho[a] = rho_new
+        active[a[done]] = False
+    relres = np.sqrt(np.divide(rr, rr0, out=np.zeros(k), where=rr0 > 0))
+    return CGResult(Z, iters, ~active, relres)
+
+
 def edge_distances(Z: np.ndarray, eu: np.ndarray, ev: np.ndarray, chunk: int = 1 << 20):
     """sum_c (Z[u, c] - Z[v, c])^2 per edge, subtracting and summing in fp64 (Eq. 6)."""
     Z = np.asarray(Z, dtype=np.float64)
@@ -145,12 +201,15 @@ class ResistanceInfo:
 
 
 def resistance(g, K: int, k_block: int, delta: float, tol: float, max_iter: int, seed: int,
-               dtype: str = "f64", col_begin: int = 0, col_end=None, L=None):
+               dtype: str = "f64", col_begin: int = 0, col_end=None, L=None,
+               precond: str = "none"):
     """R_hat over columns [col_begin, col_end) of the K-column sketch (Algorithm 1).
 
     Columns are processed in batches of at most ``k_block``; each batch forms Y,
-    runs CG and adds its squared edge distances to R before the next batch starts.
+    runs CG (or, with precond="jacobi", the Jacobi-preconditioned variant) and adds
+    its squared edge distances to R before the next batch starts.
     """
+    solve = {"none": cg_columns, "jacobi": pcg_columns}[precond]
     col_end = K if col_end is None else col_end
     GR.check_graph(g)
     L = GR.laplacian(g) if L is None else L
@@ -160,7 +219,7 @@ def resistance(g, K: int, k_block: int, delta: float, tol: float, max_iter: int,
     for c0 in range(col_begin, col_end, k_block):
         nc = min(k_block, col_end - c0)
         Y = rhs(g, K, c0, nc, seed, dtype)
-        res = cg_columns(L, delta, Y, tol, max_iter)
+        res = solve(L, delta, Y, tol, max_iter)
         R += edge_distances(res.Z, eu, ev)
         info.iters.append(res.iters)
         info.converged.append(res.converged)
