@@ -82,6 +82,12 @@ typedef struct {
 /* Time every SpMM launch with a pair of HIP events on the caller's stream and report
  * the sum in erc_solve_info.ms_spmm / spmm_timed (adds two event records per launch). */
 #define ERC_PROFILE_SPMM 2u
+/* Solve with Jacobi-preconditioned CG (M^-1 = diag(1 / (d_i + delta)), d_i = sum_j w_ij)
+ * instead of the paper's plain column-wise CG (Section 3.1.3).  Same stopping test
+ * (||r|| <= tol ||y|| on the unpreconditioned residual) and outputs; on graphs with
+ * widely spread degrees it needs far fewer iterations.  A variant, not the paper's
+ * method: results equal the plain solve only up to the CG truncation error. */
+#define ERC_JACOBI 4u
 
 /* Parameters of one resistance sweep (Algorithm 1, Require line).
  *  K_total     total projection dimension K; the JL scale is 1/sqrt(K_total) even when
@@ -98,7 +104,7 @@ typedef struct {
  *  check_every iterations enqueued between host convergence polls (0 = default 16);
  *              results do not depend on it
  *  seed        projection seed
- *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM, or 0 */
+ *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI, or 0 */
 typedef struct {
   int32_t K_total;
   int32_t k_block;

@@ -120,8 +120,11 @@ class Graph:
 
     @staticmethod
     def params(K, k_block, delta, tol, max_iter=10000, seed=0, col_begin=0, col_end=None,
-               accumulate=False, check_every=0, profile=False):
-        flags = (ERC_ACCUMULATE if accumulate else 0) | (ERC_PROFILE_SPMM if profile else 0)
+               accumulate=False, check_every=0, profile=False, precond="none"):
+        if precond not in ("none", "jacobi"):
+            raise ValueError(f"precond must be 'none' or 'jacobi', not {precond!r}")
+        flags = ((ERC_ACCUMULATE if accumulate else 0) | (ERC_PROFILE_SPMM if profile else 0)
+                 | (_abi.ERC_JACOBI if precond == "jacobi" else 0))
         return _abi.erc_solve_params(
             K_total=K, k_block=k_block, col_begin=col_begin, col_end=K if col_end is None else col_end,
             delta=delta, tol=tol, max_iter=max_iter, check_every=check_every, seed=seed,
@@ -129,14 +132,15 @@ class Graph:
 
     def resistance(self, K, k_block, delta, tol, max_iter=10000, seed=0, col_begin=0, col_end=None,
                    out=None, accumulate=False, check_every=0, raise_not_converged=True,
-                   profile=False):
-        """R (torch fp64, m) over columns [col_begin, col_end) and the solve info dict."""
+                   profile=False, precond="none"):
+        """R (torch fp64, m) over columns [col_begin, col_end) and the solve info dict.
+        precond="jacobi" selects the Jacobi-preconditioned CG variant."""
         torch = self.torch
         R = out if out is not None else torch.empty(max(self.m, 1), dtype=torch.float64,
                                                     device=self.device)
         ws = self.workspace(k_block)
         prm = self.params(K, k_block, delta, tol, max_iter, seed, col_begin, col_end, accumulate,
-                          check_every, profile)
+                          check_every, profile, precond)
         info = _abi.erc_resistance(self.handle, prm, ws.data_ptr(), ws.numel(), R.data_ptr(),
                                    self._stream(), raise_not_converged)
         return R[: self.m], info.as_dict()
@@ -226,10 +230,10 @@ class Graph:
         return Y
 
     def debug_solve_block(self, K, k_block, delta, tol, seed, col0, ncols, max_iter=10000,
-                          raise_not_converged=True):
+                          raise_not_converged=True, precond="none"):
         Z = self.torch.empty((self.n, ncols), dtype=self.vdtype, device=self.device)
         ws = self.workspace(k_block)
-        prm = self.params(K, k_block, delta, tol, max_iter, seed)
+        prm = self.params(K, k_block, delta, tol, max_iter, seed, precond=precond)
         iters, st = _abi.erc_debug_solve_block(self.handle, prm, col0, ncols, ws.data_ptr(),
                                                ws.numel(), Z.data_ptr(), self._stream(),
                                                raise_not_converged)

@@ -28,6 +28,7 @@ ERC_NODES = 0
 ERC_EDGES = 1
 ERC_ACCUMULATE = 1
 ERC_PROFILE_SPMM = 2
+ERC_JACOBI = 4
 
 
 class erc_graph_desc(ctypes.Structure):

@@ -34,6 +34,7 @@ struct DevGraph {
   const double* sw;          // m, sqrt(w_e) rounded once from fp64(w_e)
   int sw_from_w;             // 1 if w holds the input weights exactly (sqrt on the fly)
   const int64_t* ubase;      // n+1, id of the first edge (u, v>u) of row u
+  const double* deg;         // n, d_i = sum_j w_ij in fp64 (diagonal of L)
 
   // SpMM plan: per-wave ranges over `light`, plus block-cooperative tasks for long rows
   int32_t grid;              // blocks of the SpMM kernel
@@ -59,7 +60,8 @@ struct DevGraph {
 
 // Per-column CG state of one block, in the workspace.
 struct ColState {
-  double* rho;      // current r.r (fp64)
+  double* rho;      // current r.r, or r.M^-1 r with the Jacobi variant (fp64)
+  double* rr;       // current r.r (stopping test and final relative residual)
   double* rho0;     // r.r of the right-hand side
   double* thr;      // tol^2 * rho0
   double* alpha;    // step of the current iteration
@@ -95,6 +97,8 @@ struct Work {
   double* part_u;    // block partials of the update launch: grid_upd x kb pairs
   Tree tree;         // tickets and levels of the small finishing launches
   double* out;       // small fp64 output area (totals for the host)
+  void* minv;        // n: 1 / (d_i + delta) in the working precision (Jacobi variant)
+  int pc;            // 1: Jacobi-preconditioned CG, 0: plain CG
   int32_t grid_rhs, grid_upd, grid_ed;
 };
 
@@ -107,6 +111,8 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
                        const void* p, const void* r, void* q, const int32_t* gate,
                        hipStream_t s);
 hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStream_t s);
+// w.minv[i] = 1 / (d_i + delta), rounded to the working precision
+hipError_t launch_minv(const DevGraph& g, const Work& w, erc_dtype dt, double delta, hipStream_t s);
 hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream_t s);
 hipError_t launch_edge_dist(const DevGraph& g, const Work& w, erc_dtype dt, double* R,
                             int accumulate, hipStream_t s);

@@ -80,7 +80,7 @@ Shape make_shape(int64_t n, int64_t nnz) {
 
 // Byte layout of the graph buffer.
 struct GraphLayout {
-  int64_t rowptr, col, w, eid, sw, ubase, light, wave_lo, task_row, task_mega, task_chunk,
+  int64_t rowptr, col, w, eid, sw, ubase, deg, light, wave_lo, task_row, task_mega, task_chunk,
       task_beg, task_end, mega_nchunk, mega_chunk0, piece_row, piece_beg, piece_end, total;
 };
 
@@ -98,6 +98,7 @@ GraphLayout graph_layout(const Shape& s, bool weighted, erc_dtype dt) {
   L.eid = take(s.nnz * 4);
   L.sw = take(s.m * 8);
   L.ubase = take((s.n + 1) * 8);
+  L.deg = take(s.n * 8);
   L.light = take(s.n * 4);
   L.wave_lo = take((static_cast<int64_t>(s.waves) + 1) * 4);
   L.task_row = take(s.ntask_max * 4);
@@ -137,6 +138,7 @@ struct Canon {
   std::vector<int32_t> eid;    // nnz
   std::vector<double> sw;      // m
   std::vector<int64_t> ubase;  // n+1
+  std::vector<double> deg;     // n: sum_j w_ij in fp64, CSR order
   std::vector<unsigned char> wstore;  // nnz weights in the working precision
 };
 
@@ -154,6 +156,7 @@ erc_status sweep(const erc_graph_desc* d, const WT* w, Canon* out) {
     out->eid.assign(nnz, -1);
     out->sw.assign(nnz / 2, 0.0);
     out->ubase.assign(n + 1, 0);
+    out->deg.assign(n, 0.0);
   }
   int64_t next_edge = 0;
   for (int64_t i = 0; i < n; ++i) {
@@ -180,6 +183,7 @@ erc_status sweep(const erc_graph_desc* d, const WT* w, Canon* out) {
           return fail(ERC_E_INVALID_GRAPH, "weights not symmetric at entry (" +
                                                std::to_string(i) + ", " + std::to_string(j) + ")");
       }
+      if (out) out->deg[i] += (w != nullptr) ? static_cast<double>(w[pos]) : 1.0;
       if (i < j) {
         if (out) {
           out->eid[pos] = static_cast<int32_t>(next_edge);
@@ -304,8 +308,9 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 
 // Workspace layout for a padded block width.
 struct WorkLayout {
-  int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rho0, thr, alpha, beta, active,
-      iters, status, n_active, upd_pending, one, part, part_u, lvl0, lvl1, lvl2, tick, out, total;
+  int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rr, rho0, thr, alpha, beta, active,
+      iters, status, n_active, upd_pending, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
+      total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
 };
 
@@ -360,6 +365,7 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.mega_dots = take(static_cast<int64_t>(h->dg.nmega) * 3 * kb * 16);
   L.mega_tick = take(static_cast<int64_t>(h->dg.nmega) * 4);
   L.rho = take(kb * 8);
+  L.rr = take(kb * 8);
   L.rho0 = take(kb * 8);
   L.thr = take(kb * 8);
   L.alpha = take(kb * 8);
@@ -370,20 +376,21 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.n_active = take(4);
   L.upd_pending = take(4);
   L.one = take(4);
-  const int64_t nval = 8 * kb;  // up to four compensated (s, c) pairs per column
+  const int64_t nval = 10 * kb;  // up to five compensated (s, c) pairs per column
   L.part = take(static_cast<int64_t>(L.grid_tree) * 6 * kb * 8);
-  L.part_u = take(static_cast<int64_t>(L.grid_upd) * 2 * kb * 8);
+  L.part_u = take(static_cast<int64_t>(L.grid_upd) * 4 * kb * 8);  // r.r and r.M^-1 r
   // the finishing launches run ceil(grid/32) <= 256 blocks; k_count_bad runs <= 2048
   L.lvl0 = take(static_cast<int64_t>(kMaxTreeGrid) * nval * 8);
   L.lvl1 = take(ceil_div(kMaxTreeGrid, kTreeFan) * nval * 8);
   L.lvl2 = take(ceil_div(kMaxTreeGrid, kTreeFan * kTreeFan) * nval * 8);
   L.tick = take(tree_ticks(kMaxTreeGrid) * 4);
   L.out = take(8 * 8);
+  L.minv = take(h->n * s);
   L.total = off;
   return L;
 }
 
-Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
+Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int pc = 0) {
   char* b = static_cast<char*>(ws);
   Work w{};
   w.kb = kb;
@@ -395,6 +402,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
   w.mega_dots = reinterpret_cast<double*>(b + L.mega_dots);
   w.mega_tick = reinterpret_cast<uint32_t*>(b + L.mega_tick);
   w.cs.rho = reinterpret_cast<double*>(b + L.rho);
+  w.cs.rr = reinterpret_cast<double*>(b + L.rr);
   w.cs.rho0 = reinterpret_cast<double*>(b + L.rho0);
   w.cs.thr = reinterpret_cast<double*>(b + L.thr);
   w.cs.alpha = reinterpret_cast<double*>(b + L.alpha);
@@ -412,6 +420,8 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L) {
   w.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
   w.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
   w.out = reinterpret_cast<double*>(b + L.out);
+  w.minv = b + L.minv;
+  w.pc = pc;
   w.grid_rhs = L.grid_rhs;
   w.grid_upd = L.grid_upd;
   w.grid_ed = L.grid_ed;
@@ -446,7 +456,7 @@ erc_status check_params(const erc_graph_s* h, const erc_solve_params* p) {
   if (!(p->tol > 0.0 && p->tol < 1.0)) return fail(ERC_E_INVALID_ARG, "tol must be in (0, 1)");
   if (p->max_iter < 1) return fail(ERC_E_INVALID_ARG, "max_iter must be >= 1");
   if (p->check_every < 0) return fail(ERC_E_INVALID_ARG, "check_every must be >= 0");
-  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM)) != 0u)
+  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI)) != 0u)
     return fail(ERC_E_INVALID_ARG, "unknown flag");
   return ERC_OK;
 }
@@ -489,6 +499,7 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
   const double inv_sqrt_k = 1.0 / std::sqrt(static_cast<double>(p->K_total));
   const uint64_t base = splitmix_first(p->seed);
   ERC_HIP(hipEventRecord(h->ev[0], s));
+  if (w.pc) ERC_HIP(launch_minv(h->dg, w, h->dt, p->delta, s));
   ERC_HIP(launch_rhs(h->dg, w, h->dt, p->K_total, col0, nc, base, inv_sqrt_k, p->tol, s));
   ERC_HIP(hipEventRecord(h->ev[1], s));
   const int check = p->check_every > 0 ? p->check_every : kDefaultCheck;
@@ -541,7 +552,7 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
   ERC_HIP(hipMemcpyAsync(hb + kb, w.cs.active, kb * 4, hipMemcpyDeviceToHost, s));
   ERC_HIP(hipMemcpyAsync(hb + 2 * kb, w.cs.status, kb * 4, hipMemcpyDeviceToHost, s));
   double* hd = reinterpret_cast<double*>(h->pinned + 8 + 4 * kb);
-  ERC_HIP(hipMemcpyAsync(hd, w.cs.rho, kb * 8, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(hd, w.cs.rr, kb * 8, hipMemcpyDeviceToHost, s));
   ERC_HIP(hipMemcpyAsync(hd + kb, w.cs.rho0, kb * 8, hipMemcpyDeviceToHost, s));
   ERC_HIP(hipStreamSynchronize(s));
   if (prof && pending >= 0 && group_count[pending] > 0) {
@@ -704,6 +715,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   chk(up(L.eid, c.eid.data(), nnz * 4));
   chk(up(L.sw, c.sw.data(), c.m * 8));
   chk(up(L.ubase, c.ubase.data(), (n + 1) * 8));
+  chk(up(L.deg, c.deg.data(), n * 8));
   chk(up(L.light, P.light.data(), static_cast<int64_t>(P.light.size()) * 4));
   chk(up(L.wave_lo, P.wave_lo.data(), static_cast<int64_t>(P.wave_lo.size()) * 4));
   const int64_t nt = static_cast<int64_t>(P.task_row.size());
@@ -734,6 +746,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   g.eid = reinterpret_cast<const int32_t*>(base + L.eid);
   g.sw = reinterpret_cast<const double*>(base + L.sw);
   g.ubase = reinterpret_cast<const int64_t*>(base + L.ubase);
+  g.deg = reinterpret_cast<const double*>(base + L.deg);
   g.grid = s.grid;
   g.light = reinterpret_cast<const int32_t*>(base + L.light);
   g.wave_lo = reinterpret_cast<const int32_t*>(base + L.wave_lo);
@@ -814,7 +827,7 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
   if (static_cast<int64_t>(ws_bytes) < L.total)
     return fail(ERC_E_WORKSPACE, "workspace smaller than erc_workspace_bytes");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, kb, ws_dev, L);
+  const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
   st = prepare_work(h, w, L, s);
   if (st != ERC_OK) return st;
   hipEvent_t t0 = nullptr, t1 = nullptr;
@@ -1220,7 +1233,7 @@ erc_status erc_debug_solve_block(erc_handle h, const erc_solve_params* params, i
   const WorkLayout L = work_layout(h, kb);
   if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, kb, ws_dev, L);
+  const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
   st = prepare_work(h, w, L, s);
   if (st != ERC_OK) return st;
   BlockStats bs;

@@ -348,10 +348,12 @@ struct SpmmArgs {
   double* part;       // grid x 3 x kb pairs: this launch's block partials
   const int32_t* gate;
   double delta;
+  const void* minv;   // Jacobi variant: 1/(d_i + delta) per row (else nullptr)
 };
 
 // q = (L + delta I) p for a block of kb = LPN*VEC columns, plus per-column p.q, r.q,
-// q.q accumulated in at least twice the working precision.  Block tasks (long rows,
+// q.q accumulated in at least twice the working precision (with the Jacobi variant the
+// last two are weighted by m_i = 1/(d_i + delta): (m r).q and (m q).q).  Block tasks (long rows,
 // split over the 4 waves of a block and, beyond one block's share, over several
 // blocks) run first; then each wave walks its own contiguous range of short rows.
 template <typename T, int LPN, bool W>
@@ -370,6 +372,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
   const T* __restrict__ Rr = static_cast<const T*>(a.r);
   T* __restrict__ Q = static_cast<T*>(a.q);
   const T* __restrict__ wgt = static_cast<const T*>(a.g.w);
+  const T* __restrict__ minv = static_cast<const T*>(a.minv);
+  const bool pc = minv != nullptr;
   const T dlt = static_cast<T>(a.delta);
 
   // p.q, r.q, q.q partials of the rows this lane's group finishes (block tasks are
@@ -385,19 +389,20 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
     for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
     stv_nt(Q + off, qv);
     const V<T> ri = ldv_nt(Rr + off);
+    const T mi = pc ? minv[i] : T(1);
     if (dst == nullptr) {
 #pragma unroll
       for (int v = 0; v < VEC; ++v) {
         ldots[v].add(pi.x[v], qv.x[v]);
-        ldots[VEC + v].add(ri.x[v], qv.x[v]);
-        ldots[2 * VEC + v].add(qv.x[v], qv.x[v]);
+        ldots[VEC + v].add(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
+        ldots[2 * VEC + v].add(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
       }
     } else {
 #pragma unroll
       for (int v = 0; v < VEC; ++v) {
         dst[sub * VEC + v] = Dot<T>::one(pi.x[v], qv.x[v]);
-        dst[KB + sub * VEC + v] = Dot<T>::one(ri.x[v], qv.x[v]);
-        dst[2 * KB + sub * VEC + v] = Dot<T>::one(qv.x[v], qv.x[v]);
+        dst[KB + sub * VEC + v] = Dot<T>::one(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
+        dst[2 * KB + sub * VEC + v] = Dot<T>::one(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
       }
     }
   };
@@ -518,11 +523,12 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
         for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
         stv_nt(Q + off, qv);
         const V<T> ri = ldv_nt(Rr + off);
+        const T mi = pc ? minv[i] : T(1);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
           ldots[v].add(pi.x[v], qv.x[v]);
-          ldots[VEC + v].add(ri.x[v], qv.x[v]);
-          ldots[2 * VEC + v].add(qv.x[v], qv.x[v]);
+          ldots[VEC + v].add(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
+          ldots[2 * VEC + v].add(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
         }
       }
     }
@@ -582,6 +588,7 @@ struct FinArgs {
   ColState cs;
   double tol2;
   int ncols;
+  int pc;            // Jacobi variant: the partials also hold y.M^-1 y
 };
 
 // Level-1 sum of one set of block partials: block b of the finishing grid adds
@@ -602,8 +609,9 @@ __device__ void level1_sum(const DDv* __restrict__ part, int nparts, int nval, D
 struct IterArgs {
   const double* part_s;  // SpMM block partials: p.q, r.q, q.q (3 kb pairs per block)
   int nparts_s;
-  const double* part_u;  // update block partials: r.r (kb pairs per block)
+  const double* part_u;  // update block partials: r.r (and r.M^-1 r): 1 or 2 kb pairs
   int nparts_u;
+  int pc;                // Jacobi variant: the update also reduced r.M^-1 r
   Tree tree;
   ColState cs;
   const double* mega_dots;
@@ -612,53 +620,61 @@ struct IterArgs {
 };
 
 // One finishing launch per CG iteration, between the SpMM and the update kernels:
-//  (1) r.r of the update of the previous iteration (if one ran): iteration count,
-//      rho, and the per-column stopping test rho' <= tol^2 rho_0;
-//  (2) p.q, r.q, q.q of this SpMM: alpha = rho / p.q and, for the direction update,
-//      rho' = ||r - alpha q||^2 expanded in double-double.
+//  (1) r.r of the update of the previous iteration (if one ran): iteration count and
+//      the per-column stopping test r.r <= tol^2 rho_0; rho = r.r, or r.M^-1 r (also
+//      reduced by the update) with the Jacobi variant;
+//  (2) p.q, r.q, q.q of this SpMM (M^-1-weighted r.q, q.q with the Jacobi variant):
+//      alpha = rho / p.q and, for the direction update, rho' = rho - 2 alpha r.q +
+//      alpha^2 q.q, i.e. the new rho expanded in double-double.
 // Reducing the two partial sets in one tree saves a launch per iteration.
 template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
   if (*a.cs.n_active == 0) return;
-  __shared__ DDv s_in[4 * KB];
-  __shared__ DDv s_out[4 * KB];
+  __shared__ DDv s_in[5 * KB];
+  __shared__ DDv s_out[5 * KB];
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
+  const int su = (a.pc ? 2 : 1) * KB;  // update values first, then the SpMM's three
   if (upd) {
-    level1_sum(reinterpret_cast<const DDv*>(a.part_u), a.nparts_u, KB, s_in);
+    level1_sum(reinterpret_cast<const DDv*>(a.part_u), a.nparts_u, su, s_in);
   } else {
-    for (int v = threadIdx.x; v < KB; v += kBlock) s_in[v] = DDv{0.0, 0.0};
+    for (int v = threadIdx.x; v < su; v += kBlock) s_in[v] = DDv{0.0, 0.0};
   }
   if (dots) {
-    level1_sum(reinterpret_cast<const DDv*>(a.part_s), a.nparts_s, 3 * KB, s_in + KB);
+    level1_sum(reinterpret_cast<const DDv*>(a.part_s), a.nparts_s, 3 * KB, s_in + su);
   } else {
-    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) s_in[KB + v] = DDv{0.0, 0.0};
+    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) s_in[su + v] = DDv{0.0, 0.0};
   }
   __syncthreads();
-  if (!tree_sum_dd(a.tree, 4 * KB, s_in, s_out)) return;
+  if (!tree_sum_dd(a.tree, su + 3 * KB, s_in, s_out)) return;
   const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
   if (dots) {
     for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
-      DDv acc = s_out[KB + v];
+      DDv acc = s_out[su + v];
       for (int mh = 0; mh < a.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
-      s_out[KB + v] = acc;
+      s_out[su + v] = acc;
     }
   }
   __syncthreads();
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     if (upd && a.cs.active[c]) {
       const double rn = dd_value(s_out[c]);
+      const double rs = a.pc ? dd_value(s_out[KB + c]) : rn;
       a.cs.iters[c] += 1;
-      a.cs.rho[c] = rn;
+      a.cs.rr[c] = rn;
+      a.cs.rho[c] = rs;
       if (!(rn > a.cs.thr[c])) {
         a.cs.active[c] = 0;
         if (!isfinite(rn)) a.cs.status[c] = 1;
+      } else if (!(rs > 0.0) || !isfinite(rs)) {
+        a.cs.active[c] = 0;
+        a.cs.status[c] = 1;
       }
     }
     if (dots && a.cs.active[c]) {
-      const double pq = dd_value(s_out[KB + c]);
-      const DDv rq = s_out[2 * KB + c];
-      const DDv qq = s_out[3 * KB + c];
+      const double pq = dd_value(s_out[su + c]);
+      const DDv rq = s_out[su + KB + c];
+      const DDv qq = s_out[su + 2 * KB + c];
       const double rho = a.cs.rho[c];
       if (!(pq > 0.0) || !isfinite(pq) || !isfinite(dd_value(rq)) || !isfinite(dd_value(qq))) {
         a.cs.active[c] = 0;
@@ -666,9 +682,10 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
         a.cs.alpha[c] = 0.0;
         a.cs.beta[c] = 0.0;
       } else {
-        // rho' = ||r - alpha q||^2 = rho - 2 alpha r.q + alpha^2 q.q, evaluated in
-        // double-double; the exact r.r of the updated r is reduced by the next launch
-        // and drives the stopping test and the next alpha.
+        // rho' = ||r - alpha q||^2 = rho - 2 alpha r.q + alpha^2 q.q (M^-1-weighted with
+        // the Jacobi variant), evaluated in double-double; the exact value for the
+        // updated r is reduced by the next launch and drives the stopping test and the
+        // next alpha.
         const double al = rho / pq;
         const DDv t1 = dd_mul_d(rq, -2.0 * al);
         const DDv t2 = dd_mul_d(dd_mul_d(qq, al), al);
@@ -700,21 +717,25 @@ struct UpdArgs {
   void* r;
   void* p;
   const void* q;
+  const void* minv;  // Jacobi variant: 1/(d_i + delta) per row
   int64_t nvec;  // n * kb / VEC
-  double* part;  // grid x kb pairs
+  double* part;  // grid x kb pairs (grid x 2 kb with the Jacobi variant)
   ColState cs;
 };
 
 // z += alpha p; r -= alpha q; p = r + beta p (active columns); rho' = r.r in at least
-// twice the working precision.  Thread x of the grid-stride loop always covers column
-// group x % CG, so each thread keeps fixed-column partials.
-template <typename T, int CG>
+// twice the working precision.  With the Jacobi variant (PC): s = m_i r, p = s + beta p
+// and the partials hold r.r then r.s.  Thread x of the grid-stride loop always covers
+// column group x % CG (and row x / CG), so each thread keeps fixed-column partials.
+template <typename T, int CG, bool PC>
 __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
   constexpr int VEC = V<T>::N;
   constexpr int KB = CG * VEC;
+  constexpr int NP = PC ? 2 : 1;
   static_assert(kBlock % CG == 0, "column groups must divide the block");
   if (*a.cs.n_active == 0) return;
-  __shared__ DDv s_part[kBlock][VEC];
+  __shared__ DDv s_part[kBlock][NP * VEC];
+  const T* __restrict__ minv = static_cast<const T*>(a.minv);
   const int cg = threadIdx.x % CG;
   T al[VEC], be[VEC];
   bool act[VEC];
@@ -726,6 +747,7 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
     act[v] = a.cs.active[c] != 0;
   }
   Dot<T> part[VEC];
+  Dot<T> part_s[PC ? VEC : 1];
   T* __restrict__ Z = static_cast<T*>(a.z);
   T* __restrict__ R = static_cast<T*>(a.r);
   T* __restrict__ P = static_cast<T*>(a.p);
@@ -751,12 +773,19 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
       const int64_t x = x0 + u * stride;
       if (x < a.nvec) {
         const int64_t o = x * VEC;
+        const T mi = PC ? minv[x / CG] : T(1);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
           z[u].x[v] += al[v] * p[u].x[v];
           r[u].x[v] -= al[v] * q[u].x[v];
-          if (act[v]) p[u].x[v] = r[u].x[v] + be[v] * p[u].x[v];
           part[v].add(r[u].x[v], r[u].x[v]);
+          if constexpr (PC) {
+            const T sv = mi * r[u].x[v];
+            part_s[v].add(r[u].x[v], sv);
+            if (act[v]) p[u].x[v] = sv + be[v] * p[u].x[v];
+          } else {
+            if (act[v]) p[u].x[v] = r[u].x[v] + be[v] * p[u].x[v];
+          }
         }
         stv_nt(Z + o, z[u]);
         stv_nt(R + o, r[u]);
@@ -765,11 +794,15 @@ __global__ __launch_bounds__(kBlock) void k_update(UpdArgs a) {
     }
   }
 #pragma unroll
-  for (int v = 0; v < VEC; ++v) s_part[threadIdx.x][v] = part[v].get();
+  for (int v = 0; v < VEC; ++v) {
+    s_part[threadIdx.x][v] = part[v].get();
+    if constexpr (PC) s_part[threadIdx.x][VEC + v] = part_s[v].get();
+  }
   __syncthreads();
-  DDv* bp = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * KB;
-  for (int c = threadIdx.x; c < KB; c += kBlock) {
-    const int g = c / VEC, v = c % VEC;
+  DDv* bp = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * NP * KB;
+  for (int c = threadIdx.x; c < NP * KB; c += kBlock) {
+    const int k = c / KB, cc = c % KB;
+    const int g = cc / VEC, v = k * VEC + cc % VEC;
     DDv acc = s_part[g][v];
     for (int t = g + CG; t < kBlock; t += CG) acc = dd_add(acc, s_part[t][v]);
     bp[c] = acc;
@@ -786,17 +819,20 @@ struct RhsArgs {
   uint64_t words;  // 64-bit sign words per edge, ceil(K/64)
   uint64_t base;   // SplitMix64 state the sign stream starts from
   double inv_sqrt_k;
-  double* part;    // grid x kb pairs
+  double* part;    // grid x kb pairs (grid x 2 kb with the Jacobi variant)
+  const void* minv;  // Jacobi variant: 1/(d_i + delta) per row
 };
 
 // One wavefront per row; lane l holds columns l, l+64, ... of the block.  The sum over
 // the row's neighbours runs in ascending CSR order in fp64 and is rounded once, so Y is
 // reproducible bit for bit.  Edge ids, neighbours and sqrt(w) are loaded 64 at a time
-// and read back with readlane, which keeps the sign-word hash wave-uniform.
-template <typename T, int KB>
+// and read back with readlane, which keeps the sign-word hash wave-uniform.  The CG
+// state starts as z = 0, r = y and p = y (p = m_i y with the Jacobi variant, PC).
+template <typename T, int KB, bool PC>
 __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
   constexpr int CPL = (KB + 63) / 64;
-  __shared__ DDv s_part[kWavesPerBlock][KB];
+  constexpr int NP = PC ? 2 : 1;
+  __shared__ DDv s_part[kWavesPerBlock][NP * KB];
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
   T* __restrict__ Z = static_cast<T*>(a.z);
@@ -804,6 +840,7 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
   T* __restrict__ Pp = static_cast<T*>(a.p);
   const bool aligned = (a.col0 & 63) == 0;
   Dot<T> r0[CPL];
+  Dot<T> s0[PC ? CPL : 1];
   const int nw = gridDim.x * kWavesPerBlock;
   for (int i = blockIdx.x * kWavesPerBlock + wv; i < a.g.n; i += nw) {
     double acc[CPL];
@@ -848,6 +885,7 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
         }
       }
     }
+    const T mi = PC ? static_cast<const T*>(a.minv)[i] : T(1);
 #pragma unroll
     for (int cl = 0; cl < CPL; ++cl) {
       const int cc = cl * 64 + lane;
@@ -855,40 +893,52 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
         const T y = (cc < a.ncols) ? static_cast<T>(acc[cl] * a.inv_sqrt_k) : T(0);
         const int64_t o = static_cast<int64_t>(i) * KB + cc;
         R[o] = y;
-        Pp[o] = y;
         Z[o] = T(0);
         r0[cl].add(y, y);
+        if constexpr (PC) {
+          const T sv = mi * y;
+          Pp[o] = sv;
+          s0[cl].add(y, sv);
+        } else {
+          Pp[o] = y;
+        }
       }
     }
   }
 #pragma unroll
   for (int cl = 0; cl < CPL; ++cl) {
     const int cc = cl * 64 + lane;
-    if (cc < KB) s_part[wv][cc] = r0[cl].get();
+    if (cc < KB) {
+      s_part[wv][cc] = r0[cl].get();
+      if constexpr (PC) s_part[wv][KB + cc] = s0[cl].get();
+    }
   }
   __syncthreads();
-  for (int c = threadIdx.x; c < KB; c += kBlock) {
+  for (int c = threadIdx.x; c < NP * KB; c += kBlock) {
     DDv acc = s_part[0][c];
 #pragma unroll
     for (int w = 1; w < kWavesPerBlock; ++w) acc = dd_add(acc, s_part[w][c]);
     s_part[0][c] = acc;
   }
   __syncthreads();
-  DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * KB;
-  for (int c = threadIdx.x; c < KB; c += kBlock) part[c] = s_part[0][c];
+  DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * NP * KB;
+  for (int c = threadIdx.x; c < NP * KB; c += kBlock) part[c] = s_part[0][c];
 }
 
-// rho_0 = y.y per column; initial CG state of the block.
+// rho_0 = y.y per column; initial CG state of the block (rho = y.M^-1 y with the
+// Jacobi variant).
 template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_rhs(FinArgs a) {
-  __shared__ DDv s_in[KB];
-  __shared__ DDv s_out[KB];
-  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, KB, a.tree, s_in, s_out))
+  __shared__ DDv s_in[2 * KB];
+  __shared__ DDv s_out[2 * KB];
+  const int nval = (a.pc ? 2 : 1) * KB;
+  if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, nval, a.tree, s_in, s_out))
     return;
   if (threadIdx.x == 0) *a.cs.upd_pending = 0;
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     const double rr = dd_value(s_out[c]);
-    a.cs.rho[c] = rr;
+    a.cs.rho[c] = a.pc ? dd_value(s_out[KB + c]) : rr;
+    a.cs.rr[c] = rr;
     a.cs.rho0[c] = rr;
     a.cs.thr[c] = a.tol2 * rr;
     a.cs.active[c] = (c < a.ncols && rr > 0.0) ? 1 : 0;
@@ -1244,6 +1294,7 @@ hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream
   f.mega_dots = w.mega_dots;
   f.nmega = g.nmega;
   f.mode = mode;
+  f.pc = w.pc;
   switch (w.kb) {
     case 8: return fin_iter_launch<8>(f, s);
     case 16: return fin_iter_launch<16>(f, s);
@@ -1257,7 +1308,10 @@ hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream
 
 template <typename T, int KB>
 static hipError_t rhs_t(const RhsArgs& a, int grid, hipStream_t s) {
-  ERC_LAUNCH((k_rhs<T, KB>), grid, s, a);
+  if (a.minv != nullptr)
+    ERC_LAUNCH((k_rhs<T, KB, true>), grid, s, a);
+  else
+    ERC_LAUNCH((k_rhs<T, KB, false>), grid, s, a);
   return hipGetLastError();
 }
 
@@ -1295,6 +1349,7 @@ hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int
   a.base = base;
   a.inv_sqrt_k = inv_sqrt_k;
   a.part = w.part;
+  a.minv = w.pc ? w.minv : nullptr;
   hipError_t e = rhs_dispatch(dt, w.kb, a, w.grid_rhs, s);
   if (e != hipSuccess) return e;
   FinArgs f;
@@ -1304,6 +1359,7 @@ hipError_t launch_rhs(const DevGraph& g, const Work& w, erc_dtype dt, int K, int
   f.cs = w.cs;
   f.tol2 = tol * tol;
   f.ncols = ncols;
+  f.pc = w.pc;
   return fin_rhs_dispatch(w.kb, f, s);
 }
 
@@ -1329,6 +1385,7 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
   a.part = w.part;
   a.gate = gate;
   a.delta = delta;
+  a.minv = w.pc ? w.minv : nullptr;
   const int lpn = (dt == ERC_F32) ? w.kb / 4 : w.kb / 2;
   if (dt == ERC_F32) {
     switch (lpn) {
@@ -1352,7 +1409,29 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
 
 template <typename T, int CG>
 static hipError_t upd_launch(const UpdArgs& a, int grid, hipStream_t s) {
-  ERC_LAUNCH((k_update<T, CG>), grid, s, a);
+  if (a.minv != nullptr)
+    ERC_LAUNCH((k_update<T, CG, true>), grid, s, a);
+  else
+    ERC_LAUNCH((k_update<T, CG, false>), grid, s, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(kBlock) void k_minv(const double* __restrict__ deg, double delta,
+                                                 T* __restrict__ minv, int64_t n) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride)
+    minv[i] = static_cast<T>(1.0 / (deg[i] + delta));
+}
+
+hipError_t launch_minv(const DevGraph& g, const Work& w, erc_dtype dt, double delta, hipStream_t s) {
+  const int grid = grid_for(g.n, kBlock, 4096);
+  if (dt == ERC_F32)
+    ERC_LAUNCH(k_minv<float>, grid, s, g.deg, delta, static_cast<float*>(w.minv),
+               static_cast<int64_t>(g.n));
+  else
+    ERC_LAUNCH(k_minv<double>, grid, s, g.deg, delta, static_cast<double*>(w.minv),
+               static_cast<int64_t>(g.n));
   return hipGetLastError();
 }
 
@@ -1362,6 +1441,7 @@ hipError_t launch_update(const DevGraph& g, const Work& w, erc_dtype dt, hipStre
   a.r = w.r;
   a.p = w.p;
   a.q = w.q;
+  a.minv = w.pc ? w.minv : nullptr;
   const int vec = (dt == ERC_F32) ? 4 : 2;
   a.nvec = static_cast<int64_t>(g.n) * w.kb / vec;
   a.part = w.part_u;
