@@ -150,6 +150,32 @@ def subgraph_draw(G, pn, pe, torch, reps: int = 5):
     return out
 
 
+def jacobi_variant(G, g, p, R_plain, torch):
+    """One step of the same path with the Jacobi-preconditioned CG variant (ERC_JACOBI;
+    not the paper's method, not part of `value`): edges/s, iterations, and how far its
+    R lies from the plain-CG R of the last timed step (both stop at the same residual
+    tolerance, so the difference is the two solves' truncation errors)."""
+    import time as _t
+
+    torch.cuda.synchronize()
+    t0 = _t.perf_counter()
+    R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed,
+                           precond="jacobi")
+    _, kk = G.curvature(R)
+    G.sampling_probs(kk, p.eta)
+    torch.cuda.synchronize()
+    sec = _t.perf_counter() - t0
+    rel = ((R - R_plain).abs() / R_plain)[::7].float()
+    q = torch.quantile(rel[: 1 << 24], torch.tensor([0.5, 0.999], device=rel.device))
+    out = {"value": g.m / sec, "unit": "edges/s", "ms_per_step": round(sec * 1e3, 1),
+           "iters_max": info["iters_max"], "iters_total": info["iters_total"],
+           "max_final_relres": info["max_final_relres"],
+           "R_rel_diff_vs_plain": {"median": float(q[0]), "p99.9": float(q[1]),
+                                   "max": float(((R - R_plain).abs() / R_plain).max())}}
+    log(f"jacobi variant: {out}")
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -159,6 +185,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-scale", type=int, default=25,
                     help="the CPU baseline runs on a 1/cpu-scale instance of the workload")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the Jacobi-preconditioned variant after the timed steps")
     ap.add_argument("--no-draw", action="store_true",
                     help="skip the subgraph-draw measurement after the timed steps")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -198,7 +226,7 @@ def main() -> int:
                                profile=profile)
         pp, kk = G.curvature(R)
         pn, pe = G.sampling_probs(kk, p.eta)
-        last["pn"], last["pe"] = pn, pe
+        last["R"], last["pn"], last["pe"] = R, pn, pe
         return info
 
     for i in range(args.warmup):
@@ -244,6 +272,7 @@ def main() -> int:
     iters_total = infos[-1]["iters_total"]
 
     draw = None if args.no_draw else subgraph_draw(G, last["pn"], last["pe"], torch)
+    variants = None if args.no_variants else {"jacobi": jacobi_variant(G, g, p, last["R"], torch)}
 
     if args.copy_probe_mib > 0:
         nb = args.copy_probe_mib << 20
@@ -286,6 +315,7 @@ def main() -> int:
         "roofline": roofline,
         "cpu_baseline": cpu,
         "subgraph_draw": draw,
+        "variants": variants,
         "solve": {"iters_max": infos[-1]["iters_max"], "iters_total": iters_total,
                   "max_final_relres": infos[-1]["max_final_relres"],
                   "ms_rhs": infos[-1]["ms_rhs"], "ms_cg": infos[-1]["ms_cg"],
