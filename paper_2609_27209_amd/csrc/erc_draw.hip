@@ -248,17 +248,23 @@ __global__ __launch_bounds__(kBlock) void k_mark(const int64_t* __restrict__ idx
 }
 
 // Walk the upper (u < v) entries of every row by edge pieces; e is the canonical id.
+// A group of kPieceLanes lanes takes one piece, so a wavefront works on several short
+// rows at once and their chains of dependent loads overlap.
+constexpr int kPieceLanes = 16;
 template <typename F>
 __device__ __forceinline__ void for_upper_entries(const DevGraph& g, F f) {
+  constexpr int kGroups = 64 / kPieceLanes;
   const int lane = threadIdx.x & 63;
-  const int64_t nw = static_cast<int64_t>(gridDim.x) * kWavesPerBlock;
-  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6);
-       t < g.npiece; t += nw) {
+  const int sub = lane % kPieceLanes;
+  const int64_t ng = static_cast<int64_t>(gridDim.x) * kWavesPerBlock * kGroups;
+  for (int64_t t = (static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + (threadIdx.x >> 6)) *
+                       kGroups + lane / kPieceLanes;
+       t < g.npiece; t += ng) {
     const int u = g.piece_row[t];
     const int64_t pb = g.piece_beg[t], pe = g.piece_end[t];
     const int64_t upos = g.rowptr[u + 1] - (g.ubase[u + 1] - g.ubase[u]);
     const int64_t ebase = g.ubase[u] + (pb - upos);
-    for (int64_t pos = pb + lane; pos < pe; pos += 64) f(u, g.col[pos], ebase + (pos - pb));
+    for (int64_t pos = pb + sub; pos < pe; pos += kPieceLanes) f(u, g.col[pos], ebase + (pos - pb));
   }
 }
 
@@ -307,7 +313,8 @@ int grid_for_items(int64_t count, int64_t cap) {
   return static_cast<int>(g < 1 ? 1 : (g > cap ? cap : g));
 }
 int grid_for_pieces(const DevGraph& g) {
-  const int64_t b = (g.npiece + kWavesPerBlock - 1) / kWavesPerBlock;
+  const int64_t per_block = kWavesPerBlock * (64 / kPieceLanes);
+  const int64_t b = (g.npiece + per_block - 1) / per_block;
   return static_cast<int>(b < 1 ? 1 : (b > 8192 ? 8192 : b));
 }
 

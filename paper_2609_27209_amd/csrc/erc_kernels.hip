@@ -86,6 +86,12 @@ __device__ __forceinline__ double readlane_f64(double x, int k) {
                               (static_cast<unsigned int>(lo)));
 }
 
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int k) {
+  const unsigned lo = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(x & 0xffffffffull), k));
+  const unsigned hi = static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(x >> 32), k));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
 // SplitMix64 output finaliser (Steele, Lea & Flood 2014).
 __device__ __forceinline__ uint64_t splitmix_final(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -825,8 +831,9 @@ struct RhsArgs {
 
 // One wavefront per row; lane l holds columns l, l+64, ... of the block.  The sum over
 // the row's neighbours runs in ascending CSR order in fp64 and is rounded once, so Y is
-// reproducible bit for bit.  Edge ids, neighbours and sqrt(w) are loaded 64 at a time
-// and read back with readlane, which keeps the sign-word hash wave-uniform.  The CG
+// reproducible bit for bit.  Neighbours, edge ids and sqrt(w) are loaded 64 at a time;
+// each lane hashes the sign words of its own entry once, and the per-entry loop reads
+// them back with readlane (one hash per entry instead of one per entry and lane).  The CG
 // state starts as z = 0, r = y and p = y (p = m_i y with the Jacobi variant, PC).
 template <typename T, int KB, bool PC>
 __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
@@ -865,20 +872,26 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
         else
           mysw = a.g.sw[mye];
       }
+      // lane l hashes the sign words of entry base + l that the block's columns need:
+      // words w0 .. w0 + NW - 1 of its edge (one more when col0 is not word-aligned)
+      uint64_t myw[CPL + 1];
+      {
+        const uint64_t ctr0 = static_cast<uint64_t>(mye) * a.words + static_cast<uint64_t>(a.col0 >> 6);
+#pragma unroll
+        for (int u = 0; u < CPL + 1; ++u)
+          myw[u] = (u < CPL || !aligned) ? splitmix_at(a.base, ctr0 + u) : 0ull;
+      }
       for (int k = 0; k < cnt; ++k) {
         const int j = __builtin_amdgcn_readlane(myj, k);
-        const int ee = __builtin_amdgcn_readlane(mye, k);
         const double s = readlane_f64(mysw, k);
         const double t = (i < j) ? s : -s;  // B_{e,i}: +1 at the smaller endpoint
-        const uint64_t ctr0 = static_cast<uint64_t>(ee) * a.words;
 #pragma unroll
         for (int cl = 0; cl < CPL; ++cl) {
           const int c = a.col0 + cl * 64 + lane;  // global column of this lane
-          const int wlo = (a.col0 + cl * 64) >> 6;
-          uint64_t word = splitmix_at(a.base, ctr0 + wlo);
+          uint64_t word = readlane_u64(myw[cl], k);
           if (!aligned) {
-            const uint64_t whi = splitmix_at(a.base, ctr0 + wlo + 1);
-            word = ((c >> 6) == wlo) ? word : whi;
+            const uint64_t whi = readlane_u64(myw[cl + 1], k);
+            word = ((c >> 6) == ((a.col0 + cl * 64) >> 6)) ? word : whi;
           }
           const bool neg = (word >> (c & 63)) & 1ull;
           acc[cl] += neg ? -t : t;
