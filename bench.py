@@ -176,6 +176,62 @@ def jacobi_variant(G, g, p, R_plain, torch):
     return out
 
 
+def per_config_table(steps: int, warmup: int):
+    """Every workload at its own solve parameters: curvature edges/s and m*K/s end to
+    end (resistance + curvature + sampling probabilities, inputs in HBM), iterations,
+    average SpMM launch, and the device memory the caller allocates (graph buffer,
+    workspace, R, p, kappa and both probability vectors, sampling scratch) for block
+    widths 32..256 (the paper's Table 3 reports peak memory against its batch size b)."""
+    import torch
+
+    import gen
+    import paper_2609_27209_amd as E
+    from paper_2609_27209_amd import _abi
+
+    rows = []
+    for name in gen.configs.ORDER:
+        wl = gen.CONFIGS[name]
+        p = wl.params
+        g = gen.make_graph(name, progress=log)
+        G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=p.dtype)
+
+        def step(profile):
+            R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed,
+                                   profile=profile)
+            _, kk = G.curvature(R)
+            G.sampling_probs(kk, p.eta)
+            return info
+
+        for _ in range(warmup):
+            step(False)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        infos = [step(True) for _ in range(steps)]
+        torch.cuda.synchronize()
+        sec = (time.perf_counter() - t0) / steps
+        full = sum(i["spmm_full"] for i in infos)
+        avg = sum(i["ms_spmm"] for i in infos) / max(full, 1)
+        kb = padded(p.k_block, p.dtype)
+        bl = spmm_bytes_per_launch(g, kb, p.dtype)
+        outputs = 8 * (2 * g.m + 3 * g.n) + _abi.erc_sampling_scratch_bytes(G.handle)
+        widths = [b for b in (32, 64, 128, 256) if p.dtype == "f32" or b <= 128]
+        desc, keep = E._desc(g.rowptr, g.col, g.w, p.dtype)
+        gbytes = _abi.erc_graph_bytes(desc)
+        del desc, keep
+        mem = {str(b): gbytes + _abi.erc_workspace_bytes(G.handle, b) + outputs for b in widths}
+        rows.append({"workload": name, "n": g.n, "m": g.m, "K": p.K, "k_block": p.k_block,
+                     "dtype": p.dtype, "ms_per_step": round(sec * 1e3, 2),
+                     "edges_per_s": g.m / sec, "edge_columns_per_s": g.m * p.K / sec,
+                     "iters_max": infos[-1]["iters_max"],
+                     "spmm_avg_ms": round(avg, 4),
+                     "spmm_algorithmic_gbs": round(bl / (avg / 1e3) / 1e9, 1) if full else None,
+                     "device_bytes_by_block_width": mem})
+        log(f"{name}: {rows[-1]}")
+        G.close()
+        del G, g
+    return {"table": "per_config", "steps": steps, "warmup": warmup, "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -187,6 +243,9 @@ def main() -> int:
                     help="the CPU baseline runs on a 1/cpu-scale instance of the workload")
     ap.add_argument("--no-variants", action="store_true",
                     help="skip the Jacobi-preconditioned variant after the timed steps")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the benchmark line: one line with every workload's "
+                         "edges/s, iterations, SpMM time and device memory per block width")
     ap.add_argument("--no-draw", action="store_true",
                     help="skip the subgraph-draw measurement after the timed steps")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -209,6 +268,9 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     torch.cuda.set_device(0)
+    if args.configs:
+        print(json.dumps(per_config_table(args.steps, args.warmup)), flush=True)
+        return 0
     wl = gen.CONFIGS[args.config]
     p = wl.params
     t0 = time.perf_counter()

@@ -284,6 +284,12 @@ __device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
 #define ERC_SPMM_INFLIGHT 8
 #endif
 constexpr int kInflight = ERC_SPMM_INFLIGHT;
+// Short-row chunks whose longest row exceeds this many entries are gathered one row at
+// a time by the whole wavefront instead of one row per lane group.
+#ifndef ERC_WAVE_ROW_MIN
+#define ERC_WAVE_ROW_MIN 32
+#endif
+constexpr int kWaveRowMin = ERC_WAVE_ROW_MIN;
 
 template <typename T, int LPN, bool W>
 __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
@@ -468,7 +474,9 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
   // 2. this wave's short rows, NPW at a time: lane group g owns row lo + g (+ NPW ...),
   // loads its own neighbour indices LPN at a time and gathers kInflight rows of p per
   // step, so a wavefront has NPW rows and NPW * kInflight gathers in flight and needs
-  // no cross-group reduction per row.
+  // no cross-group reduction per row.  A chunk whose longest row has more than
+  // kWaveRowMin entries would leave the other groups idle; its rows are gathered one at
+  // a time by the whole wavefront instead.
   {
     constexpr int NPW = 64 / LPN;
     const int grp = lane / LPN;
@@ -481,11 +489,25 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
       const int i = valid ? a.g.light[k] : a.g.light[lo];
       const int64_t b = a.g.rowptr[i];
       const int deg = valid ? static_cast<int>(a.g.rowptr[i + 1] - b) : 0;
-      const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
-      V<T> acc = vzero<T>();
       int dmax = deg;
 #pragma unroll
       for (int off = LPN; off < 64; off <<= 1) dmax = max(dmax, __shfl_xor(dmax, off));
+      if (dmax > kWaveRowMin) {
+        // a chunk with a long row: the whole wavefront takes its rows one at a time
+        const int kn = min(NPW, hi - k0);
+        for (int r = 0; r < kn; ++r) {
+          const int ir = a.g.light[k0 + r];
+          const V<T> pir = ldv(P + static_cast<int64_t>(ir) * KB + sub * VEC);
+          V<T> accr = vzero<T>();
+          gather_row<T, LPN, W>(a.g.col, wgt, P, ir, a.g.rowptr[ir], a.g.rowptr[ir + 1], pir,
+                                accr, lane);
+          reduce_groups<T, LPN>(accr);
+          if (lane < LPN) finish(ir, pir, accr, nullptr);
+        }
+        continue;
+      }
+      const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
+      V<T> acc = vzero<T>();
       for (int base = 0; base < dmax; base += LPN) {
         const int t = base + sub;
         int myj = i;
