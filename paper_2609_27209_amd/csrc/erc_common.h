@@ -71,6 +71,9 @@ struct ColState {
   int32_t* status;  // 0 ok, 1 breakdown
   int32_t* n_active;  // one int: number of active columns (polled by the host)
   int32_t* upd_pending;  // one int: an update ran whose r.r is not yet reduced
+  int32_t* pred_done;  // one int: every active column is predicted to stop after the
+                       // pending update, so its exact test runs before the next SpMM
+  int32_t* nspmm;      // one int: SpMM launches of this block that found active columns
   int32_t* one;       // one int holding 1 (keeps debug launches from exiting early)
 };
 

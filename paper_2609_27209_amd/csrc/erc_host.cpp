@@ -309,7 +309,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 // Workspace layout for a padded block width.
 struct WorkLayout {
   int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rr, rho0, thr, alpha, beta, active,
-      iters, status, n_active, upd_pending, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
+      iters, status, n_active, upd_pending, pred_done, nspmm, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
       total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
 };
@@ -375,6 +375,8 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.status = take(kb * 4);
   L.n_active = take(4);
   L.upd_pending = take(4);
+  L.pred_done = take(4);
+  L.nspmm = take(4);
   L.one = take(4);
   const int64_t nval = 10 * kb;  // up to five compensated (s, c) pairs per column
   L.part = take(static_cast<int64_t>(L.grid_tree) * 6 * kb * 8);
@@ -412,6 +414,8 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
   w.cs.status = reinterpret_cast<int32_t*>(b + L.status);
   w.cs.n_active = reinterpret_cast<int32_t*>(b + L.n_active);
   w.cs.upd_pending = reinterpret_cast<int32_t*>(b + L.upd_pending);
+  w.cs.pred_done = reinterpret_cast<int32_t*>(b + L.pred_done);
+  w.cs.nspmm = reinterpret_cast<int32_t*>(b + L.nspmm);
   w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
   w.part = reinterpret_cast<double*>(b + L.part);
   w.part_u = reinterpret_cast<double*>(b + L.part_u);
@@ -522,6 +526,9 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
       if (prof) ERC_HIP(hipEventRecord(pr[1], s));
       ERC_HIP(launch_fin_iter(h->dg, w, 0, s));
       ERC_HIP(launch_update(h->dg, w, h->dt, s));
+      // the exact stopping test, only when every column is predicted to stop: saves
+      // the SpMM that would otherwise run after the last update
+      ERC_HIP(launch_fin_iter(h->dg, w, 2, s));
     }
     group_count[slot] = nb;
     done += nb;
@@ -554,16 +561,14 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
   double* hd = reinterpret_cast<double*>(h->pinned + 8 + 4 * kb);
   ERC_HIP(hipMemcpyAsync(hd, w.cs.rr, kb * 8, hipMemcpyDeviceToHost, s));
   ERC_HIP(hipMemcpyAsync(hd + kb, w.cs.rho0, kb * 8, hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipMemcpyAsync(h->pinned + 2, w.cs.nspmm, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   ERC_HIP(hipStreamSynchronize(s));
   if (prof && pending >= 0 && group_count[pending] > 0) {
     erc_status pst = read_prof(h, pending, group_count[pending], st);
     if (pst != ERC_OK) return pst;
   }
-  int32_t block_max = 0;
-  for (int c = 0; c < nc; ++c) block_max = std::max(block_max, hb[c]);
-  // SpMM launches that found an active column: one per iteration plus the one that
-  // precedes the finishing launch which detects the last convergence
-  st->spmm_full += std::min<int64_t>(block_max + 1, done);
+  // SpMM launches that found an active column (counted on the device)
+  st->spmm_full += h->pinned[2];
   for (int c = 0; c < nc; ++c) {
     const int32_t it = hb[c];
     st->iters_total += it;

@@ -644,7 +644,9 @@ struct IterArgs {
   ColState cs;
   const double* mega_dots;
   int nmega;
-  int mode;              // 0: stopping test of the pending update, then alpha/beta; 1: test only
+  int mode;              // 0: stopping test of the pending update, then alpha/beta; 1: test
+                         // only; 2: test only, and only when the previous mode-0 launch
+                         // predicted that every active column stops
 };
 
 // One finishing launch per CG iteration, between the SpMM and the update kernels:
@@ -658,8 +660,10 @@ struct IterArgs {
 template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
   if (*a.cs.n_active == 0) return;
+  if (a.mode == 2 && *a.cs.pred_done == 0) return;
   __shared__ DDv s_in[5 * KB];
   __shared__ DDv s_out[5 * KB];
+  __shared__ int s_live[KB];
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
   const int su = (a.pc ? 2 : 1) * KB;  // update values first, then the SpMM's three
@@ -685,6 +689,7 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
   }
   __syncthreads();
   for (int c = threadIdx.x; c < KB; c += kBlock) {
+    s_live[c] = 0;
     if (upd && a.cs.active[c]) {
       const double rn = dd_value(s_out[c]);
       const double rs = a.pc ? dd_value(s_out[KB + c]) : rn;
@@ -720,6 +725,9 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
         const double rf = dd_value(dd_add(dd_add(DDv{rho, 0.0}, t1), t2));
         a.cs.alpha[c] = al;
         a.cs.beta[c] = (rf > 0.0 ? rf : 0.0) / rho;
+        // plain CG: rf predicts the r.r of the stopping test; with the Jacobi variant
+        // it is r.M^-1 r, so every column counts as possibly stopping
+        s_live[c] = (!a.pc && rf > a.cs.thr[c]) ? 1 : 0;
       }
     } else {
       a.cs.alpha[c] = 0.0;
@@ -728,10 +736,15 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int cnt = 0;
-    for (int c = 0; c < KB; ++c) cnt += a.cs.active[c] != 0;
+    int cnt = 0, live = 0;
+    for (int c = 0; c < KB; ++c) {
+      cnt += a.cs.active[c] != 0;
+      live |= s_live[c];
+    }
     *a.cs.n_active = cnt;
     *a.cs.upd_pending = (dots && cnt > 0) ? 1 : 0;
+    *a.cs.pred_done = (dots && cnt > 0 && !live) ? 1 : 0;
+    if (dots) *a.cs.nspmm += 1;
   }
 }
 
@@ -969,7 +982,11 @@ __global__ __launch_bounds__(kBlock) void k_fin_rhs(FinArgs a) {
   const int nval = (a.pc ? 2 : 1) * KB;
   if (!reduce_partials(reinterpret_cast<const DDv*>(a.part), a.nparts, nval, a.tree, s_in, s_out))
     return;
-  if (threadIdx.x == 0) *a.cs.upd_pending = 0;
+  if (threadIdx.x == 0) {
+    *a.cs.upd_pending = 0;
+    *a.cs.pred_done = 0;
+    *a.cs.nspmm = 0;
+  }
   for (int c = threadIdx.x; c < KB; c += kBlock) {
     const double rr = dd_value(s_out[c]);
     a.cs.rho[c] = a.pc ? dd_value(s_out[KB + c]) : rr;
