@@ -74,6 +74,9 @@ struct ColState {
   int32_t* pred_done;  // one int: every active column is predicted to stop after the
                        // pending update, so its exact test runs before the next SpMM
   int32_t* nspmm;      // one int: SpMM launches of this block that found active columns
+  uint32_t* fin_cnt;   // finishing-step counters: active columns, predicted-live flag and
+  uint32_t* fin_live;  // the blocks done; zero between launches
+  uint32_t* fin_tick;
   int32_t* one;       // one int holding 1 (keeps debug launches from exiting early)
 };
 

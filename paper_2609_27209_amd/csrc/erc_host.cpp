@@ -309,7 +309,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 // Workspace layout for a padded block width.
 struct WorkLayout {
   int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rr, rho0, thr, alpha, beta, active,
-      iters, status, n_active, upd_pending, pred_done, nspmm, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
+      iters, status, n_active, upd_pending, pred_done, nspmm, fin_ctr, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
       total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
 };
@@ -377,6 +377,7 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.upd_pending = take(4);
   L.pred_done = take(4);
   L.nspmm = take(4);
+  L.fin_ctr = take(3 * 4);
   L.one = take(4);
   const int64_t nval = 10 * kb;  // up to five compensated (s, c) pairs per column
   L.part = take(static_cast<int64_t>(L.grid_tree) * 6 * kb * 8);
@@ -416,6 +417,9 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
   w.cs.upd_pending = reinterpret_cast<int32_t*>(b + L.upd_pending);
   w.cs.pred_done = reinterpret_cast<int32_t*>(b + L.pred_done);
   w.cs.nspmm = reinterpret_cast<int32_t*>(b + L.nspmm);
+  w.cs.fin_cnt = reinterpret_cast<uint32_t*>(b + L.fin_ctr);
+  w.cs.fin_live = w.cs.fin_cnt + 1;
+  w.cs.fin_tick = w.cs.fin_cnt + 2;
   w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
   w.part = reinterpret_cast<double*>(b + L.part);
   w.part_u = reinterpret_cast<double*>(b + L.part_u);
@@ -437,6 +441,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
 erc_status prepare_work(const erc_graph_s* h, const Work& w, const WorkLayout& L, hipStream_t s) {
   ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(kMaxTreeGrid), s));
   ERC_HIP(launch_fill_u32(w.mega_tick, 0u, h->dg.nmega, s));
+  ERC_HIP(launch_fill_u32(w.cs.fin_cnt, 0u, 3, s));
   ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.one), 1u, 1, s));
   return ERC_OK;
 }

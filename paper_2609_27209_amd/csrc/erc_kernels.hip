@@ -649,50 +649,107 @@ struct IterArgs {
                          // predicted that every active column stops
 };
 
-// One finishing launch per CG iteration, between the SpMM and the update kernels:
-//  (1) r.r of the update of the previous iteration (if one ran): iteration count and
-//      the per-column stopping test r.r <= tol^2 rho_0; rho = r.r, or r.M^-1 r (also
-//      reduced by the update) with the Jacobi variant;
-//  (2) p.q, r.q, q.q of this SpMM (M^-1-weighted r.q, q.q with the Jacobi variant):
-//      alpha = rho / p.q and, for the direction update, rho' = rho - 2 alpha r.q +
-//      alpha^2 q.q, i.e. the new rho expanded in double-double.
-// Reducing the two partial sets in one tree saves a launch per iteration.
+// The per-iteration finishing step, in two launches without device-scope fences:
+//  k_fin_sum  (ceil(parts/32) blocks) level-1 sums of the block partials of the
+//             previous update (r.r, and r.M^-1 r with the Jacobi variant) and of this
+//             SpMM (p.q, r.q, q.q; M^-1-weighted r.q, q.q with the Jacobi variant),
+//             stored value-major so that the next launch reads them contiguously;
+//             skipped when the partial sets are short (k_fin_col then reads them);
+//  k_fin_col  (one block per column) the grid totals of its column in a fixed order,
+//             then (1) the stopping test of the pending update, r.r <= tol^2 rho_0,
+//             and rho = r.r (or r.M^-1 r), and (2) alpha = rho / p.q and, for the
+//             direction update, rho' = rho - 2 alpha r.q + alpha^2 q.q, i.e. the new rho
+//             expanded in double-double.  Integer atomics collect the active-column
+//             count; the last block to finish publishes it.
+// mode 0: both steps; 1: the stopping test only; 2: the stopping test only, and only
+// when the previous mode-0 step predicted that every active column stops.
+constexpr int kFinDirectMax = 1024;  // longest partial set k_fin_col sums by itself
+
 template <int KB>
-__global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
+__global__ __launch_bounds__(kBlock) void k_fin_sum(IterArgs a) {
   if (*a.cs.n_active == 0) return;
   if (a.mode == 2 && *a.cs.pred_done == 0) return;
-  __shared__ DDv s_in[5 * KB];
-  __shared__ DDv s_out[5 * KB];
-  __shared__ int s_live[KB];
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
   const int su = (a.pc ? 2 : 1) * KB;  // update values first, then the SpMM's three
-  if (upd) {
-    level1_sum(reinterpret_cast<const DDv*>(a.part_u), a.nparts_u, su, s_in);
-  } else {
-    for (int v = threadIdx.x; v < su; v += kBlock) s_in[v] = DDv{0.0, 0.0};
-  }
-  if (dots) {
-    level1_sum(reinterpret_cast<const DDv*>(a.part_s), a.nparts_s, 3 * KB, s_in + su);
-  } else {
-    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) s_in[su + v] = DDv{0.0, 0.0};
-  }
-  __syncthreads();
-  if (!tree_sum_dd(a.tree, su + 3 * KB, s_in, s_out)) return;
-  const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
-  if (dots) {
-    for (int v = threadIdx.x; v < 3 * KB; v += kBlock) {
-      DDv acc = s_out[su + v];
-      for (int mh = 0; mh < a.nmega; ++mh) acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB + v]);
-      s_out[su + v] = acc;
+  const int nval = su + 3 * KB;
+  DDv* l0 = reinterpret_cast<DDv*>(a.tree.lvl0);
+  const int b0 = blockIdx.x * kTreeFan;
+  for (int v = threadIdx.x; v < nval; v += kBlock) {
+    const bool isu = v < su;
+    const DDv* part = reinterpret_cast<const DDv*>(isu ? a.part_u : a.part_s);
+    const int np = isu ? a.nparts_u : a.nparts_s;
+    const int pv = isu ? su : 3 * KB;
+    const int vv = isu ? v : v - su;
+    const int nb = min(kTreeFan, np - b0);
+    DDv acc = DDv{0.0, 0.0};
+    if ((isu ? upd : dots) && nb > 0) {
+      acc = part[static_cast<int64_t>(b0) * pv + vv];
+      for (int k = 1; k < nb; ++k) acc = dd_add(acc, part[static_cast<int64_t>(b0 + k) * pv + vv]);
     }
+    l0[static_cast<int64_t>(v) * gridDim.x + blockIdx.x] = acc;
+  }
+}
+
+// nsum > 0: k_fin_sum wrote nsum level-1 sums per value; nsum == 0: read the block
+// partials themselves.
+template <int KB>
+__global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
+  if (*a.cs.n_active == 0) return;
+  if (a.mode == 2 && *a.cs.pred_done == 0) return;
+  __shared__ DDv s_red[5][kBlock];
+  __shared__ int s_last;
+  const bool upd = *a.cs.upd_pending != 0;
+  const bool dots = a.mode == 0;
+  const int su = (a.pc ? 2 : 1) * KB;
+  const int nval = su + 3 * KB;
+  const int c = blockIdx.x;
+  const int tid = threadIdx.x;
+  // value slots of this column: r.r, r.M^-1 r, p.q, r.q, q.q
+  const int idx[5] = {c, KB + c, su + c, su + KB + c, su + 2 * KB + c};
+#pragma unroll
+  for (int k = 0; k < 5; ++k) {
+    const bool need = (k == 0 && upd) || (k == 1 && upd && a.pc) || (k >= 2 && dots);
+    // element t of this value's list: a level-1 sum, or one block's partial
+    const DDv* src;
+    int64_t stride;
+    int cnt;
+    if (nsum > 0) {
+      src = reinterpret_cast<const DDv*>(a.tree.lvl0) + static_cast<int64_t>(idx[k]) * nsum;
+      stride = 1;
+      cnt = nsum;
+    } else if (k < 2) {
+      src = reinterpret_cast<const DDv*>(a.part_u) + idx[k];
+      stride = su;
+      cnt = a.nparts_u;
+    } else {
+      src = reinterpret_cast<const DDv*>(a.part_s) + (idx[k] - su);
+      stride = 3 * KB;
+      cnt = a.nparts_s;
+    }
+    DDv acc = DDv{0.0, 0.0};
+    if (need) {
+      for (int t = tid; t < cnt; t += kBlock) {
+        const DDv x = src[static_cast<int64_t>(t) * stride];
+        acc = (t == tid) ? x : dd_add(acc, x);
+      }
+    }
+    s_red[k][tid] = acc;
   }
   __syncthreads();
-  for (int c = threadIdx.x; c < KB; c += kBlock) {
-    s_live[c] = 0;
+  for (int w = kBlock / 2; w > 0; w >>= 1) {
+    if (tid < w) {
+#pragma unroll
+      for (int k = 0; k < 5; ++k) s_red[k][tid] = dd_add(s_red[k][tid], s_red[k][tid + w]);
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
+    int live = 0;
     if (upd && a.cs.active[c]) {
-      const double rn = dd_value(s_out[c]);
-      const double rs = a.pc ? dd_value(s_out[KB + c]) : rn;
+      const double rn = dd_value(s_red[0][0]);
+      const double rs = a.pc ? dd_value(s_red[1][0]) : rn;
       a.cs.iters[c] += 1;
       a.cs.rr[c] = rn;
       a.cs.rho[c] = rs;
@@ -705,9 +762,14 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
       }
     }
     if (dots && a.cs.active[c]) {
-      const double pq = dd_value(s_out[su + c]);
-      const DDv rq = s_out[su + KB + c];
-      const DDv qq = s_out[su + 2 * KB + c];
+      DDv pqd = s_red[2][0], rq = s_red[3][0], qq = s_red[4][0];
+      for (int mh = 0; mh < a.nmega; ++mh) {
+        const DDv* m = md + static_cast<int64_t>(mh) * 3 * KB;
+        pqd = dd_add(pqd, m[c]);
+        rq = dd_add(rq, m[KB + c]);
+        qq = dd_add(qq, m[2 * KB + c]);
+      }
+      const double pq = dd_value(pqd);
       const double rho = a.cs.rho[c];
       if (!(pq > 0.0) || !isfinite(pq) || !isfinite(dd_value(rq)) || !isfinite(dd_value(qq))) {
         a.cs.active[c] = 0;
@@ -717,8 +779,8 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
       } else {
         // rho' = ||r - alpha q||^2 = rho - 2 alpha r.q + alpha^2 q.q (M^-1-weighted with
         // the Jacobi variant), evaluated in double-double; the exact value for the
-        // updated r is reduced by the next launch and drives the stopping test and the
-        // next alpha.
+        // updated r is reduced by the next finishing step and drives the stopping test
+        // and the next alpha.
         const double al = rho / pq;
         const DDv t1 = dd_mul_d(rq, -2.0 * al);
         const DDv t2 = dd_mul_d(dd_mul_d(qq, al), al);
@@ -727,24 +789,25 @@ __global__ __launch_bounds__(kBlock) void k_fin_iter(IterArgs a) {
         a.cs.beta[c] = (rf > 0.0 ? rf : 0.0) / rho;
         // plain CG: rf predicts the r.r of the stopping test; with the Jacobi variant
         // it is r.M^-1 r, so every column counts as possibly stopping
-        s_live[c] = (!a.pc && rf > a.cs.thr[c]) ? 1 : 0;
+        live = (!a.pc && rf > a.cs.thr[c]) ? 1 : 0;
       }
     } else {
       a.cs.alpha[c] = 0.0;
       a.cs.beta[c] = 0.0;
     }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int cnt = 0, live = 0;
-    for (int c = 0; c < KB; ++c) {
-      cnt += a.cs.active[c] != 0;
-      live |= s_live[c];
+    if (a.cs.active[c]) atomicAdd(a.cs.fin_cnt, 1u);
+    if (live) atomicOr(a.cs.fin_live, 1u);
+    s_last = atomicAdd(a.cs.fin_tick, 1u) == static_cast<unsigned>(gridDim.x - 1);
+    if (s_last) {
+      // every other block has added its column: publish the totals, reset the counters
+      const int cnt = static_cast<int>(atomicExch(a.cs.fin_cnt, 0u));
+      const bool any_live = atomicExch(a.cs.fin_live, 0u) != 0u;
+      atomicExch(a.cs.fin_tick, 0u);
+      *a.cs.n_active = cnt;
+      *a.cs.upd_pending = (dots && cnt > 0) ? 1 : 0;
+      *a.cs.pred_done = (dots && cnt > 0 && !any_live) ? 1 : 0;
+      if (dots) *a.cs.nspmm += 1;
     }
-    *a.cs.n_active = cnt;
-    *a.cs.upd_pending = (dots && cnt > 0) ? 1 : 0;
-    *a.cs.pred_done = (dots && cnt > 0 && !live) ? 1 : 0;
-    if (dots) *a.cs.nspmm += 1;
   }
 }
 
@@ -1319,7 +1382,10 @@ static hipError_t fin_rhs_launch(const FinArgs& f, hipStream_t s) {
 template <int KB>
 static hipError_t fin_iter_launch(const IterArgs& f, hipStream_t s) {
   const int np = f.nparts_s > f.nparts_u ? f.nparts_s : f.nparts_u;
-  ERC_LAUNCH((k_fin_iter<KB>), (np + kTreeFan - 1) / kTreeFan, s, f);
+  // short partial sets are summed by k_fin_col directly (one launch instead of two)
+  const int nsum = np > kFinDirectMax ? (np + kTreeFan - 1) / kTreeFan : 0;
+  if (nsum > 0) ERC_LAUNCH((k_fin_sum<KB>), nsum, s, f);
+  ERC_LAUNCH((k_fin_col<KB>), KB, s, f, nsum);
   return hipGetLastError();
 }
 
