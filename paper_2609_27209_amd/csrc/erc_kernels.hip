@@ -619,21 +619,6 @@ struct FinArgs {
   int pc;            // Jacobi variant: the partials also hold y.M^-1 y
 };
 
-// Level-1 sum of one set of block partials: block b of the finishing grid adds
-// partials [32 b, 32 b + 32) of the set in order (none past its end).
-__device__ void level1_sum(const DDv* __restrict__ part, int nparts, int nval, DDv* dst) {
-  const int b0 = blockIdx.x * kTreeFan;
-  const int nb = min(kTreeFan, nparts - b0);
-  for (int v = threadIdx.x; v < nval; v += blockDim.x) {
-    DDv acc = DDv{0.0, 0.0};
-    if (nb > 0) {
-      acc = part[static_cast<int64_t>(b0) * nval + v];
-      for (int k = 1; k < nb; ++k) acc = dd_add(acc, part[static_cast<int64_t>(b0 + k) * nval + v]);
-    }
-    dst[v] = acc;
-  }
-}
-
 struct IterArgs {
   const double* part_s;  // SpMM block partials: p.q, r.q, q.q (3 kb pairs per block)
   int nparts_s;
@@ -1092,23 +1077,34 @@ __global__ __launch_bounds__(kBlock) void k_edge_dist(DevGraph g, const T* __res
     const V<T> zu = ldv(Z + static_cast<int64_t>(u) * KB + sub * VEC);
     for (int64_t base = pb; base < pe; base += 64) {
       const int cnt = static_cast<int>(min(static_cast<int64_t>(64), pe - base));
+      const int64_t e0 = ebase + (base - pb);
+      // this window's neighbours and (when accumulating) their previous R, one
+      // coalesced load each; then kInflight neighbour rows of z in flight per lane
       const int myj = (lane < cnt) ? g.col[base + lane] : u;
+      const double myr = (accumulate && lane < cnt) ? R[e0 + lane] : 0.0;
       const int steps = (cnt + NPW - 1) / NPW;
-      for (int st = 0; st < steps; ++st) {
-        const int k = st * NPW + grp;
-        const int j = __shfl(myj, k);
-        const V<T> zv = ldv(Z + static_cast<int64_t>(j) * KB + sub * VEC);
-        double d = 0.0;
+      for (int st0 = 0; st0 < steps; st0 += kInflight) {
+        V<T> zv[kInflight];
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-          const double df = static_cast<double>(zu.x[v]) - static_cast<double>(zv.x[v]);
-          d += df * df;
+        for (int q = 0; q < kInflight; ++q) {
+          const int k = (st0 + q) * NPW + grp;
+          int j = __shfl(myj, k & 63);
+          if (k >= cnt) j = u;
+          zv[q] = ldv(Z + static_cast<int64_t>(j) * KB + sub * VEC);
         }
 #pragma unroll
-        for (int off = 1; off < LPN; off <<= 1) d += __shfl_xor(d, off);
-        if (sub == 0 && k < cnt) {
-          const int64_t ed = ebase + (base - pb) + k;
-          R[ed] = accumulate ? R[ed] + d : d;
+        for (int q = 0; q < kInflight; ++q) {
+          const int k = (st0 + q) * NPW + grp;
+          double d = 0.0;
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) {
+            const double df = static_cast<double>(zu.x[v]) - static_cast<double>(zv[q].x[v]);
+            d += df * df;
+          }
+#pragma unroll
+          for (int off = 1; off < LPN; off <<= 1) d += __shfl_xor(d, off);
+          const double r0 = __shfl(myr, k & 63);
+          if (sub == 0 && k < cnt) R[e0 + k] = accumulate ? r0 + d : d;
         }
       }
     }
