@@ -254,8 +254,8 @@ def main() -> int:
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the column "
-              "sharding over several GPUs is described in DESIGN.md but not built.",
-              file=sys.stderr)
+              "sharding over several GPUs (a range of columns per GPU, then one sum of R) "
+              "is not built.", file=sys.stderr)
         return 2
 
     import numpy as np
