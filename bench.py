@@ -213,7 +213,8 @@ def per_config_table(steps: int, warmup: int):
         avg = sum(i["ms_spmm"] for i in infos) / max(full, 1)
         kb = padded(p.k_block, p.dtype)
         bl = spmm_bytes_per_launch(g, kb, p.dtype)
-        outputs = 8 * (2 * g.m + 3 * g.n) + _abi.erc_sampling_scratch_bytes(G.handle)
+        # R, kappa and edge probabilities (m fp64 each); p and node probabilities (n each)
+        outputs = 8 * (3 * g.m + 2 * g.n) + _abi.erc_sampling_scratch_bytes(G.handle)
         widths = [b for b in (32, 64, 128, 256) if p.dtype == "f32" or b <= 128]
         desc, keep = E._desc(g.rowptr, g.col, g.w, p.dtype)
         gbytes = _abi.erc_graph_bytes(desc)
