@@ -24,7 +24,8 @@ _L = None
 def _work(args):
     c0, c1, prm, path = args
     R, info = erc.resistance(_G, prm["K"], prm["k_block"], prm["delta"], prm["tol"],
-                             prm["max_iter"], prm["seed"], prm["dtype"], c0, c1, L=_L)
+                             prm["max_iter"], prm["seed"], prm["dtype"], c0, c1, L=_L,
+                             precond=prm["precond"])
     np.save(path, R)
     iters = np.concatenate(info.iters) if info.iters else np.zeros(0, np.int64)
     conv = np.concatenate(info.converged) if info.converged else np.zeros(0, bool)
@@ -32,7 +33,7 @@ def _work(args):
 
 
 def resistance_parallel(g, K, k_block, delta, tol, max_iter, seed, dtype="f64", col_begin=0,
-                        col_end=None, procs=None, progress=None):
+                        col_end=None, procs=None, progress=None, precond="none"):
     """R over columns [col_begin, col_end), solved in `procs` column ranges.
 
     Returns (R, iters, converged) with per-column iteration counts and flags in column
@@ -48,7 +49,7 @@ def resistance_parallel(g, K, k_block, delta, tol, max_iter, seed, dtype="f64", 
     _G = g
     _L = GR.laplacian(g)
     prm = dict(K=K, k_block=k_block, delta=delta, tol=tol, max_iter=max_iter, seed=seed,
-               dtype=dtype)
+               dtype=dtype, precond=precond)
     with tempfile.TemporaryDirectory(prefix="erc_oracle_") as tmp:
         jobs = [(bounds[k], bounds[k + 1], prm, os.path.join(tmp, f"R{k}.npy"))
                 for k in range(procs)]

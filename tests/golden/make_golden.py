@@ -1,11 +1,13 @@
 """Write the stored oracle values used by the large-workload parity tests.
 
-    python tests/golden/make_golden.py cl170k [cl230k cl2400k ...]
+    python tests/golden/make_golden.py cl170k [cl230k cl2400k cl2400k:jacobi ...]
 
 Each run regenerates the seeded graph, runs the CPU oracle (column-parallel, see
 oracle/parallel.py) over the workload's full projection, or over the column range
 named in RANGES, then computes curvature and sampling probabilities from that R and
 stores the values at seeded samples of edges and nodes in tests/golden/<name>.npz.
+A name with the suffix ":jacobi" solves with the oracle's Jacobi-preconditioned CG
+instead and writes tests/golden/<name>_jacobi.npz.
 Only gen/ and oracle/ are used; nothing here touches the GPU library.  The full oracle
 R is cached under $TMPDIR so the stored fields can be recomputed without the solve.
 
@@ -45,10 +47,10 @@ def log(msg):
     print(f"[golden] {msg}", flush=True)
 
 
-def cache_path(name):
+def cache_path(tag):
     d = os.path.join(os.environ.get("TMPDIR", "/tmp"), "erc_golden_cache")
     os.makedirs(d, exist_ok=True)
-    return os.path.join(d, f"{name}_R_v{ORACLE_VERSION}.npz")
+    return os.path.join(d, f"{tag}_R_v{ORACLE_VERSION}.npz")
 
 
 def sampling_bounds(g, R, kappa, s, node_prob, edge_prob, eta):
@@ -70,14 +72,17 @@ def sampling_bounds(g, R, kappa, s, node_prob, edge_prob, eta):
     return S, bound_node, bound_edge, kmin, kmax
 
 
-def make(name, procs):
+def make(spec, procs):
+    name, _, precond = spec.partition(":")
+    precond = precond or "none"
+    tag = name if precond == "none" else f"{name}_{precond}"
     wl = gen.CONFIGS[name]
     p = wl.params
     t0 = time.time()
     g = gen.make_graph(name, progress=log)
     log(f"{name}: graph {g.summary()} ({time.time() - t0:.0f}s)")
     c0, c1 = RANGES.get(name, (0, p.K))
-    cp = cache_path(name)
+    cp = cache_path(tag)
     if os.path.exists(cp):
         with np.load(cp) as f:
             R, iters, conv, t_solve = f["R"], f["iters"], f["conv"], float(f["t_solve"])
@@ -85,7 +90,8 @@ def make(name, procs):
     else:
         t0 = time.time()
         R, iters, conv = resistance_parallel(g, p.K, p.k_block, p.delta, p.tol, p.max_iter,
-                                             p.seed, p.dtype, c0, c1, procs=procs, progress=log)
+                                             p.seed, p.dtype, c0, c1, procs=procs, progress=log,
+                                             precond=precond)
         t_solve = time.time() - t0
         np.savez(cp, R=R, iters=iters, conv=conv, t_solve=t_solve)
     log(f"{name}: resistance over columns [{c0}, {c1}) in {t_solve:.0f}s, "
@@ -106,12 +112,13 @@ def make(name, procs):
     meta = {"workload": name, "graph": g.summary(), "col_begin": c0, "col_end": c1,
             "K": p.K, "k_block": p.k_block, "delta": p.delta, "tol": p.tol, "seed": p.seed,
             "dtype": p.dtype, "eta": p.eta, "oracle_version": ORACLE_VERSION, "rtol": RTOL,
+            "precond": precond,
             "solve_seconds": round(t_solve, 1), "procs": procs,
             "iters_min": int(iters.min()), "iters_max": int(iters.max()),
             "iters_total": int(iters.sum()), "converged": bool(conv.all()),
             "kappa_min": kmin, "kappa_max": kmax,
             "components": OG.components(g)}
-    out = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"{name}.npz")
+    out = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"{tag}.npz")
     np.savez_compressed(
         out, meta=np.array(json.dumps(meta)), edge_idx=es, node_idx=ns,
         R=R[es], kappa=kappa[es], kappa_scale=S[es], edge_prob=edge_prob[es],
