@@ -383,6 +383,9 @@ def main() -> int:
                   "max_final_relres": infos[-1]["max_final_relres"],
                   "ms_rhs": infos[-1]["ms_rhs"], "ms_cg": infos[-1]["ms_cg"],
                   "ms_accum": infos[-1]["ms_accum"],
+                  "bytes_model": infos[-1]["bytes_model"],
+                  "model_gbs": round(infos[-1]["bytes_model"] / (infos[-1]["ms_total"] / 1e3)
+                                     / 1e9, 1),
                   "edge_columns_per_s": g.m * p.K / (ms_per_step / 1000.0)},
     }
     print(json.dumps(line), flush=True)

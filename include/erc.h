@@ -136,6 +136,10 @@ typedef struct {
   int64_t spmm_timed;         /* with ERC_PROFILE_SPMM: SpMM launches timed          */
   int64_t spmm_full;          /* SpMM launches that found an active column (the rest
                                  return at once after convergence)                   */
+  double bytes_model;         /* algorithmic HBM bytes of the call: per SpMM and update
+                                 that found active columns, one pass over every array
+                                 they read or write (neighbour gathers counted once),
+                                 plus right-hand sides and edge distances per block   */
 } erc_solve_info;
 
 /* ---- graph ---------------------------------------------------------------------- */

@@ -48,7 +48,8 @@ class erc_solve_info(ctypes.Structure):
                 ("breakdowns", c_int32), ("iters_total", c_int64), ("launches", c_int64),
                 ("nonpositive", c_int64), ("max_final_relres", c_double), ("ms_rhs", c_float),
                 ("ms_cg", c_float), ("ms_accum", c_float), ("ms_total", c_float),
-                ("ms_spmm", c_float), ("spmm_timed", c_int64), ("spmm_full", c_int64)]
+                ("ms_spmm", c_float), ("spmm_timed", c_int64), ("spmm_full", c_int64),
+                ("bytes_model", c_double)]
 
     def as_dict(self) -> dict:
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -890,6 +890,24 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     info->ms_spmm = bs.ms_spmm;
     info->spmm_timed = bs.spmm_timed;
     info->spmm_full = bs.spmm_full;
+    // algorithmic bytes (no neighbour-row gathers beyond one read of each vector): every
+    // SpMM that found active columns reads col (+ w), rowptr, p and r and writes q; its
+    // update reads z, r, p, q and writes z, r, p; per block the right-hand sides read
+    // col, eid (+ w) and write z, r, p, and the edge distances read the upper col
+    // entries and z and read-modify-write R
+    {
+      const double sz = static_cast<double>(dsize(h->dt));
+      const double n = static_cast<double>(h->n), nnz = static_cast<double>(h->nnz);
+      const double m = static_cast<double>(h->m);
+      const double kb = static_cast<double>(padded_width(h->dt, params->k_block));
+      const double wb = h->weighted ? sz : 0.0;
+      const double spmm = (4.0 + wb) * nnz + 8.0 * (n + 1) + 3.0 * sz * n * kb;
+      const double upd = 7.0 * sz * n * kb;
+      const double rhs = (8.0 + wb) * nnz + 3.0 * sz * n * kb;
+      const double ed = 2.0 * nnz + sz * n * kb + 16.0 * m;
+      info->bytes_model = static_cast<double>(bs.spmm_full) * (spmm + upd) +
+                          static_cast<double>(blocks) * (rhs + ed);
+    }
   }
   if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown in " + std::to_string(bs.breakdowns) + " column(s)");
   if (bad > 0) return fail(ERC_E_NUMERIC, std::to_string(bad) + " resistance(s) <= 0 or not finite");

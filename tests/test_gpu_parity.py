@@ -251,3 +251,20 @@ def test_invalid_arguments_raise():
         G.resistance(32, 32, -1.0, 1e-8, 100, 1)       # delta <= 0
     with pytest.raises(E.ErcError):
         G.resistance(32, 32, 1e-6, 1e-8, 100, 1, col_begin=10, col_end=5)
+
+
+def test_solve_info_byte_model():
+    # the documented algorithmic byte model of erc_solve_info.bytes_model
+    E = _gpu()
+    g = gen.make_graph("sbm20k")
+    p = gen.CONFIGS["sbm20k"].params
+    G = _graph(E, g, p.dtype)
+    R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed)
+    s, kb, n, nnz, m = 4, 64, g.n, g.nnz, g.m
+    spmm = (4 + s) * nnz + 8 * (n + 1) + 3 * s * n * kb
+    upd = 7 * s * n * kb
+    rhs = (8 + s) * nnz + 3 * s * n * kb
+    ed = 2 * nnz + s * n * kb + 16 * m
+    want = info["spmm_full"] * (spmm + upd) + info["blocks"] * (rhs + ed)
+    assert info["spmm_full"] >= info["iters_max"]
+    assert info["bytes_model"] == pytest.approx(want, rel=1e-12)
