@@ -481,7 +481,7 @@ struct BlockStats {
 erc_status ensure_prof_events(erc_graph_s* h, int check) {
   if (h->prof_check >= check) return ERC_OK;
   for (auto& e : h->prof)
-    if (e) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
   h->prof.assign(static_cast<size_t>(4) * check, nullptr);
   for (auto& e : h->prof) ERC_HIP(hipEventCreate(&e));
   h->prof_check = check;
@@ -699,9 +699,9 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   h->shape = s;
   for (int64_t i = 0; i < n; ++i) h->nonisolated += desc->rowptr[i + 1] > desc->rowptr[i];
   auto cleanup = [&](erc_status e) {
-    if (h->pinned) hipHostFree(h->pinned);
+    if (h->pinned) (void)hipHostFree(h->pinned);
     for (auto& ev : h->ev)
-      if (ev) hipEventDestroy(ev);
+      if (ev) (void)hipEventDestroy(ev);
     delete h;
     return e;
   };
@@ -805,11 +805,11 @@ erc_status erc_edge_endpoints(erc_handle h, int32_t* u_dev, int32_t* v_dev, void
 erc_status erc_destroy(erc_handle h) {
   g_last_error.clear();
   if (h == nullptr) return ERC_OK;
-  if (h->pinned) hipHostFree(h->pinned);
+  if (h->pinned) (void)hipHostFree(h->pinned);
   for (auto& ev : h->ev)
-    if (ev) hipEventDestroy(ev);
+    if (ev) (void)hipEventDestroy(ev);
   for (auto& ev : h->prof)
-    if (ev) hipEventDestroy(ev);
+    if (ev) (void)hipEventDestroy(ev);
   delete h;
   return ERC_OK;
 }
@@ -851,8 +851,8 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     const int acc = (c0 == params->col_begin && !(params->flags & ERC_ACCUMULATE)) ? 0 : 1;
     st = solve_block(h, params, w, c0, nc, h->m > 0 ? R_dev : nullptr, acc, nullptr, &bs, s);
     if (st != ERC_OK) {
-      hipEventDestroy(t0);
-      hipEventDestroy(t1);
+      (void)hipEventDestroy(t0);
+      (void)hipEventDestroy(t1);
       return st;
     }
     ++blocks;
@@ -871,9 +871,9 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     ERC_HIP(hipStreamSynchronize(s));
   }
   float total = 0.0f;
-  hipEventElapsedTime(&total, t0, t1);
-  hipEventDestroy(t0);
-  hipEventDestroy(t1);
+  (void)hipEventElapsedTime(&total, t0, t1);  // timing only: 0 if unavailable
+  (void)hipEventDestroy(t0);
+  (void)hipEventDestroy(t1);
   if (info) {
     info->blocks = blocks;
     info->iters_max = bs.iters_max;
