@@ -306,8 +306,8 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
     int myj = i;
     T myw = T(0);
     if (lane < cnt) {
-      myj = __builtin_nontemporal_load(col + base + lane);
-      if (W) myw = __builtin_nontemporal_load(wgt + base + lane);
+      myj = col[base + lane];
+      if (W) myw = wgt[base + lane];
     }
     const int steps = (cnt + NPW - 1) / NPW;
     for (int st = 0; st < steps; st += kInflight) {
@@ -513,8 +513,8 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
         int myj = i;
         T myw = T(0);
         if (t < deg) {
-          myj = __builtin_nontemporal_load(a.g.col + b + t);
-          if (W) myw = __builtin_nontemporal_load(wgt + b + t);
+          myj = a.g.col[b + t];
+          if (W) myw = wgt[b + t];
         }
         const int cnt = min(LPN, dmax - base);
         for (int u0 = 0; u0 < cnt; u0 += kInflight) {
