@@ -36,8 +36,11 @@ from oracle import erc as OE  # noqa: E402
 from oracle import graph as OG  # noqa: E402
 from oracle.parallel import resistance_parallel  # noqa: E402
 
-# column ranges for workloads whose full sketch is too long for the CPU oracle
-RANGES = {"cl2400k": (0, 64)}
+# column ranges for workloads whose full sketch is too long for the CPU oracle: on the
+# 2.4M-node graph one column-iteration of the fp64 oracle takes several seconds and a
+# column needs ~540 iterations, so the stored range is the first 16 columns (the GPU
+# solves them in a 64-column block, the launch configuration of the benchmark)
+RANGES = {"cl2400k": (0, 16)}
 SAMPLES = 8192
 RTOL = 1e-4
 ORACLE_VERSION = 2  # bump when the oracle's arithmetic changes
