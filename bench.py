@@ -179,7 +179,8 @@ def jacobi_variant(G, g, p, R_plain, torch):
 def per_config_table(steps: int, warmup: int):
     """Every workload at its own solve parameters: curvature edges/s and m*K/s end to
     end (resistance + curvature + sampling probabilities, inputs in HBM), iterations,
-    average SpMM launch, and the device memory the caller allocates (graph buffer,
+    average SpMM launch, one step of the Jacobi variant (time and iterations; one run,
+    after the timed steps), and the device memory the caller allocates (graph buffer,
     workspace, R, p, kappa and both probability vectors, sampling scratch) for block
     widths 32..256 (the paper's Table 3 reports peak memory against its batch size b)."""
     import torch
@@ -216,6 +217,15 @@ def per_config_table(steps: int, warmup: int):
         # R, kappa and edge probabilities (m fp64 each); p and node probabilities (n each)
         outputs = 8 * (3 * g.m + 2 * g.n) + _abi.erc_sampling_scratch_bytes(G.handle)
         widths = [b for b in (32, 64, 128, 256) if p.dtype == "f32" or b <= 128]
+        torch.cuda.synchronize()
+        tj = time.perf_counter()
+        Rj, ij = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed,
+                              precond="jacobi")
+        _, kj = G.curvature(Rj)
+        G.sampling_probs(kj, p.eta)
+        torch.cuda.synchronize()
+        sec_j = time.perf_counter() - tj
+        del Rj, kj
         desc, keep = E._desc(g.rowptr, g.col, g.w, p.dtype)
         gbytes = _abi.erc_graph_bytes(desc)
         del desc, keep
@@ -226,7 +236,9 @@ def per_config_table(steps: int, warmup: int):
                      "iters_max": infos[-1]["iters_max"],
                      "spmm_avg_ms": round(avg, 4),
                      "spmm_algorithmic_gbs": round(bl / (avg / 1e3) / 1e9, 1) if full else None,
-                     "device_bytes_by_block_width": mem})
+                     "device_bytes_by_block_width": mem,
+                     "jacobi": {"ms_per_step": round(sec_j * 1e3, 2),
+                                "iters_max": ij["iters_max"]}})
         log(f"{name}: {rows[-1]}")
         G.close()
         del G, g
