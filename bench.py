@@ -245,6 +245,53 @@ def per_config_table(steps: int, warmup: int):
     return {"table": "per_config", "steps": steps, "warmup": warmup, "rows": rows}
 
 
+def block_sweep(name: str, widths):
+    """The paper's Table 3 experiment on one workload: the same resistance + curvature +
+    sampling-probability step at several block widths b (columns per CG block; K, the
+    shift, the tolerance and the seed unchanged), one step each after one warm-up block:
+    ms per step, iterations, average SpMM launch and its algorithmic rate, and the
+    device memory the caller allocates at that b (graph buffer, workspace, outputs,
+    sampling scratch)."""
+    import torch
+
+    import gen
+    import paper_2609_27209_amd as E
+    from paper_2609_27209_amd import _abi
+
+    wl = gen.CONFIGS[name]
+    p = wl.params
+    g = gen.make_graph(name, progress=log)
+    G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=p.dtype)
+    desc, keep = E._desc(g.rowptr, g.col, g.w, p.dtype)
+    gbytes = _abi.erc_graph_bytes(desc)
+    del desc, keep
+    outputs = 8 * (3 * g.m + 2 * g.n) + _abi.erc_sampling_scratch_bytes(G.handle)
+    G.resistance(p.K, widths[0], p.delta, p.tol, p.max_iter, p.seed, col_begin=0,
+                 col_end=widths[0])
+    rows = []
+    for b in widths:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        R, info = G.resistance(p.K, b, p.delta, p.tol, p.max_iter, p.seed, profile=True)
+        _, kk = G.curvature(R)
+        G.sampling_probs(kk, p.eta)
+        torch.cuda.synchronize()
+        sec = time.perf_counter() - t0
+        avg = info["ms_spmm"] / max(info["spmm_full"], 1)
+        bl = spmm_bytes_per_launch(g, padded(b, p.dtype), p.dtype)
+        rows.append({"k_block": b, "blocks": info["blocks"], "ms_per_step": round(sec * 1e3, 1),
+                     "edges_per_s": g.m / sec, "iters_max": info["iters_max"],
+                     "iters_total": info["iters_total"], "spmm_launches": info["spmm_full"],
+                     "spmm_avg_ms": round(avg, 4),
+                     "spmm_algorithmic_gbs": round(bl / (avg / 1e3) / 1e9, 1),
+                     "device_bytes": gbytes + _abi.erc_workspace_bytes(G.handle, b) + outputs})
+        log(f"{name} b={b}: {rows[-1]}")
+        del R, kk
+    G.close()
+    return {"table": "block_sweep", "workload": name, "n": g.n, "m": g.m, "K": p.K,
+            "dtype": p.dtype, "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +306,10 @@ def main() -> int:
     ap.add_argument("--configs", action="store_true",
                     help="instead of the benchmark line: one line with every workload's "
                          "edges/s, iterations, SpMM time and device memory per block width")
+    ap.add_argument("--block-sweep", default=None, metavar="B,B,...",
+                    help="instead of the benchmark line: one line with the --config "
+                         "workload's step time, iterations and device memory at each of "
+                         "these block widths")
     ap.add_argument("--no-draw", action="store_true",
                     help="skip the subgraph-draw measurement after the timed steps")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -283,6 +334,10 @@ def main() -> int:
     torch.cuda.set_device(0)
     if args.configs:
         print(json.dumps(per_config_table(args.steps, args.warmup)), flush=True)
+        return 0
+    if args.block_sweep:
+        widths = [int(b) for b in args.block_sweep.split(",")]
+        print(json.dumps(block_sweep(args.config, widths)), flush=True)
         return 0
     wl = gen.CONFIGS[args.config]
     p = wl.params
