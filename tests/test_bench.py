@@ -1,0 +1,106 @@
+"""bench.py's contract: one JSON line with the fields the benchmark driver reads, the
+roofline and CPU-baseline objects, the block-width sweep, and a refusal of more than one
+GPU.  The GPU cases run bench.main() in this process on the 20,000-node workload."""
+import json
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import gen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def _main(monkeypatch, *args):
+    monkeypatch.setattr(sys, "argv", ["bench.py", *args])
+    return bench.main()
+
+
+def test_refuses_more_than_one_gpu(monkeypatch, capsys):
+    assert _main(monkeypatch, "--gpus", "2") == 2
+    cap = capsys.readouterr()
+    assert cap.out == ""
+    assert "one GPU" in cap.err
+
+
+def test_padded_widths():
+    assert [bench.padded(k, "f32") for k in (1, 16, 17, 64, 100, 256)] == [16, 16, 32, 64, 128, 256]
+    assert [bench.padded(k, "f64") for k in (1, 8, 9, 128)] == [8, 8, 16, 128]
+
+
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "f64"])
+def test_spmm_byte_model_reads_each_array_once(weighted, dtype):
+    g = gen.erdos_renyi(300, 0.03, 7, weighted=weighted)
+    kb = 32
+    vt = np.float32 if dtype == "f32" else np.float64
+    # the arrays one launch streams: column indices, weights in the working precision,
+    # row pointers, and the n x kb blocks p (read), r (read) and q (written)
+    arrays = [g.col.astype(np.int32), g.rowptr.astype(np.int64)]
+    if weighted:
+        arrays.append(np.asarray(g.w).astype(vt))
+    block = np.zeros((g.n, kb), dtype=vt)
+    expect = sum(a.nbytes for a in arrays) + 3 * block.nbytes
+    assert bench.spmm_bytes_per_launch(g, kb, dtype) == expect
+
+
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+@pytest.mark.gpu
+def test_bench_line(monkeypatch, capsys):
+    _gpu()
+    assert _main(monkeypatch, "--config", "sbm20k", "--steps", "2", "--warmup", "1",
+                 "--no-variants") == 0
+    lines = capsys.readouterr().out.strip().splitlines()
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for k in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step",
+              "higher_is_better", "scaling", "vs_baseline", "dtype", "data", "config",
+              "roofline", "cpu_baseline"):
+        assert k in d, k
+    assert (d["n_gpus"], d["steps"], d["warmup"]) == (1, 2, 1)
+    assert d["higher_is_better"] is True and d["vs_baseline"] is None
+    assert d["config"]["workload"] == "sbm20k" and d["dtype"] == "f32"
+    g = gen.make_graph("sbm20k")
+    assert math.isclose(d["value"], g.m / (d["ms_per_step"] / 1e3), rel_tol=1e-6)
+    r = d["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert 0.0 < r["frac"] < 1.0
+    assert math.isclose(r["frac"], r["achieved"] / r["peak"], abs_tol=1e-4)
+    # avg_launch_ms is printed to 4 decimals
+    assert math.isclose(r["achieved"], r["bytes_per_launch"] / (r["avg_launch_ms"] / 1e3) / 1e9,
+                        rel_tol=1e-3 + 0.5e-4 / r["avg_launch_ms"])
+    assert r["traffic"] is None  # counters were taken on the 2.4M-node workload only
+    c = d["cpu_baseline"]
+    assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["sample"]
+    assert d["subgraph_draw"]["edges"]["draws"] == max(1, g.m // 1000)
+
+
+@pytest.mark.gpu
+def test_block_sweep(monkeypatch, capsys):
+    _gpu()
+    assert _main(monkeypatch, "--config", "sbm20k", "--block-sweep", "16,32,64") == 0
+    lines = capsys.readouterr().out.strip().splitlines()
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    assert d["table"] == "block_sweep" and d["workload"] == "sbm20k"
+    rows = d["rows"]
+    assert [r["k_block"] for r in rows] == [16, 32, 64]
+    assert [r["blocks"] for r in rows] == [4, 2, 1]  # K = 64
+    mem = [r["device_bytes"] for r in rows]
+    assert mem[0] < mem[1] < mem[2]
+    # the workspace holds the n x b blocks z, r, p, q (fp32) and per-column partials
+    n = gen.make_graph("sbm20k").n
+    for k in (1, 2):
+        assert mem[k] - mem[0] >= 4 * n * (rows[k]["k_block"] - rows[0]["k_block"]) * 4
+    assert all(r["ms_per_step"] > 0 and r["iters_max"] > 0 for r in rows)
