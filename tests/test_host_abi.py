@@ -79,6 +79,10 @@ def _raw_desc(n, rowptr, col, w=None, wdt=_abi.ERC_F32, sdt=_abi.ERC_F32):
     ("nan_weight", _abi.ERC_E_INVALID_GRAPH),
     ("asymmetric_weight", _abi.ERC_E_INVALID_GRAPH),
     ("zero_nodes", _abi.ERC_E_INVALID_ARG),
+    ("n_at_limit", _abi.ERC_E_INVALID_ARG),
+    ("nnz_at_limit", _abi.ERC_E_INVALID_GRAPH),
+    ("bad_solve_dtype", _abi.ERC_E_INVALID_ARG),
+    ("bad_weight_dtype", _abi.ERC_E_INVALID_ARG),
 ])
 def test_validate_rejects(case, expect):
     # base graph: path 0-1-2 (rows 0:[1] 1:[0,2] 2:[1])
@@ -105,7 +109,15 @@ def test_validate_rejects(case, expect):
         w = np.array([1.0, 1.5, 2.0, 2.0], np.float32)
     elif case == "zero_nodes":
         n, rp, col, w = 0, [0], [0], None
-    d, keep = _raw_desc(n, rp, col, w)
+    elif case == "n_at_limit":
+        # n = 2^31 is refused before rowptr is read
+        n, rp, col, w = 1 << 31, [0], [0], None
+    elif case == "nnz_at_limit":
+        # rowptr[n] = 2^31 is refused before col is read
+        n, rp, col, w = 1, [0, 1 << 31], [0], None
+    d, keep = _raw_desc(n, rp, col, w,
+                        sdt=7 if case == "bad_solve_dtype" else _abi.ERC_F32,
+                        wdt=7 if case == "bad_weight_dtype" else _abi.ERC_F32)
     assert _status(_abi.erc_validate, d) == expect
     assert _abi.erc_last_error() != ""
 
