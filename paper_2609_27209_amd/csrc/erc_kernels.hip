@@ -669,8 +669,19 @@ __global__ __launch_bounds__(kBlock) void k_fin_sum(IterArgs a) {
     const int nb = min(kTreeFan, np - b0);
     DDv acc = DDv{0.0, 0.0};
     if ((isu ? upd : dots) && nb > 0) {
-      acc = part[static_cast<int64_t>(b0) * pv + vv];
-      for (int k = 1; k < nb; ++k) acc = dd_add(acc, part[static_cast<int64_t>(b0 + k) * pv + vv]);
+      // partials in block order; eight loads are issued before they are added, so the
+      // sum is the same as one at a time
+      const DDv* src = part + static_cast<int64_t>(b0) * pv + vv;
+      acc = src[0];
+      int k = 1;
+      for (; k + 8 <= nb; k += 8) {
+        DDv x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = src[static_cast<int64_t>(k + u) * pv];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = dd_add(acc, x[u]);
+      }
+      for (; k < nb; ++k) acc = dd_add(acc, src[static_cast<int64_t>(k) * pv]);
     }
     l0[static_cast<int64_t>(v) * gridDim.x + blockIdx.x] = acc;
   }
@@ -718,6 +729,12 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
         const DDv x = src[static_cast<int64_t>(t) * stride];
         acc = (t == tid) ? x : dd_add(acc, x);
       }
+      // the SpMM dots of rows split over several blocks (one triple of pairs per row)
+      if (k >= 2) {
+        const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots) + (k - 2) * KB + c;
+        for (int mh = tid; mh < a.nmega; mh += kBlock)
+          acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB]);
+      }
     }
     s_red[k][tid] = acc;
   }
@@ -730,7 +747,6 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
     __syncthreads();
   }
   if (tid == 0) {
-    const DDv* md = reinterpret_cast<const DDv*>(a.mega_dots);
     int live = 0;
     if (upd && a.cs.active[c]) {
       const double rn = dd_value(s_red[0][0]);
@@ -747,13 +763,7 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
       }
     }
     if (dots && a.cs.active[c]) {
-      DDv pqd = s_red[2][0], rq = s_red[3][0], qq = s_red[4][0];
-      for (int mh = 0; mh < a.nmega; ++mh) {
-        const DDv* m = md + static_cast<int64_t>(mh) * 3 * KB;
-        pqd = dd_add(pqd, m[c]);
-        rq = dd_add(rq, m[KB + c]);
-        qq = dd_add(qq, m[2 * KB + c]);
-      }
+      const DDv pqd = s_red[2][0], rq = s_red[3][0], qq = s_red[4][0];
       const double pq = dd_value(pqd);
       const double rho = a.cs.rho[c];
       if (!(pq > 0.0) || !isfinite(pq) || !isfinite(dd_value(rq)) || !isfinite(dd_value(qq))) {
