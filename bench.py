@@ -32,8 +32,8 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 # the kernel source it was measured on: reported as null once that file changes.
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
-    "kernel_sha256_16": "a5d4e59214e42600",
-    "fetch_bytes": 32679538488,
+    "kernel_sha256_16": "7de81ee34ce09d06",
+    "fetch_bytes": 32678171480,
     "write_bytes": 639565824,
     "profile": "profiles/k_spmm_cl2400k.md",
 }
