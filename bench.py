@@ -32,8 +32,8 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 # the kernel source it was measured on: reported as null once that file changes.
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
-    "kernel_sha256_16": "7de81ee34ce09d06",
-    "fetch_bytes": 32678171480,
+    "kernel_sha256_16": "90db047141efc012",
+    "fetch_bytes": 32598712307,
     "write_bytes": 639565824,
     "profile": "profiles/k_spmm_cl2400k.md",
 }

@@ -22,6 +22,14 @@ constexpr int kMaxTreeGrid = 2048;
 
 // Device view of the graph operator (all pointers are device memory inside the
 // caller's graph buffer).
+// A light row of the SpMM plan with its CSR range, so that one 16-byte load gives a
+// lane group everything it needs to start on the row.
+struct alignas(16) LightRow {
+  int64_t beg;  // rowptr[row]
+  int32_t row;
+  int32_t deg;  // rowptr[row + 1] - rowptr[row]
+};
+
 struct DevGraph {
   int32_t n;
   int64_t nnz;
@@ -38,7 +46,7 @@ struct DevGraph {
 
   // SpMM plan: per-wave ranges over `light`, plus block-cooperative tasks for long rows
   int32_t grid;              // blocks of the SpMM kernel
-  const int32_t* light;      // light rows, ascending
+  const LightRow* light;     // light rows, ascending, with their CSR ranges
   const int32_t* wave_lo;    // grid*4 + 1 boundaries into `light`
   int32_t ntask;             // block tasks (task t runs on block t % grid)
   const int32_t* task_row;

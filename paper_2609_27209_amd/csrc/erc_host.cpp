@@ -99,7 +99,7 @@ GraphLayout graph_layout(const Shape& s, bool weighted, erc_dtype dt) {
   L.sw = take(s.m * 8);
   L.ubase = take((s.n + 1) * 8);
   L.deg = take(s.n * 8);
-  L.light = take(s.n * 4);
+  L.light = take(s.n * static_cast<int64_t>(sizeof(LightRow)));
   L.wave_lo = take((static_cast<int64_t>(s.waves) + 1) * 4);
   L.task_row = take(s.ntask_max * 4);
   L.task_mega = take(s.ntask_max * 4);
@@ -726,7 +726,12 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   chk(up(L.sw, c.sw.data(), c.m * 8));
   chk(up(L.ubase, c.ubase.data(), (n + 1) * 8));
   chk(up(L.deg, c.deg.data(), n * 8));
-  chk(up(L.light, P.light.data(), static_cast<int64_t>(P.light.size()) * 4));
+  std::vector<LightRow> lrows(P.light.size());
+  for (size_t k = 0; k < P.light.size(); ++k) {
+    const int32_t i = P.light[k];
+    lrows[k] = LightRow{desc->rowptr[i], i, static_cast<int32_t>(desc->rowptr[i + 1] - desc->rowptr[i])};
+  }
+  chk(up(L.light, lrows.data(), static_cast<int64_t>(lrows.size() * sizeof(LightRow))));
   chk(up(L.wave_lo, P.wave_lo.data(), static_cast<int64_t>(P.wave_lo.size()) * 4));
   const int64_t nt = static_cast<int64_t>(P.task_row.size());
   chk(up(L.task_row, P.task_row.data(), nt * 4));
@@ -758,7 +763,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
   g.ubase = reinterpret_cast<const int64_t*>(base + L.ubase);
   g.deg = reinterpret_cast<const double*>(base + L.deg);
   g.grid = s.grid;
-  g.light = reinterpret_cast<const int32_t*>(base + L.light);
+  g.light = reinterpret_cast<const LightRow*>(base + L.light);
   g.wave_lo = reinterpret_cast<const int32_t*>(base + L.wave_lo);
   g.ntask = static_cast<int32_t>(nt);
   g.task_row = reinterpret_cast<const int32_t*>(base + L.task_row);

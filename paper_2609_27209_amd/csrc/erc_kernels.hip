@@ -369,7 +369,9 @@ struct SpmmArgs {
 // split over the 4 waves of a block and, beyond one block's share, over several
 // blocks) run first; then each wave walks its own contiguous range of short rows.
 template <typename T, int LPN, bool W>
-__global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
+// At most 128 VGPRs (four waves per SIMD): the 32-column instantiation would take 138
+// and fall to three waves, which costs more than its few spilled registers.
+__global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   constexpr int VEC = V<T>::N;
   constexpr int KB = LPN * VEC;
   if (*a.gate == 0) return;
@@ -483,12 +485,20 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
     const int gw = blockIdx.x * kWavesPerBlock + wv;
     const int lo = a.g.wave_lo[gw];
     const int hi = a.g.wave_lo[gw + 1];
+    const LightRow* __restrict__ LR = a.g.light;
+    // each group's next light row is loaded one step ahead, so a step starts with the
+    // row id and CSR range at hand; groups past the end repeat the wave's last row
+    // with no entries
+    LightRow nxt{};
+    if (lo < hi) nxt = LR[min(lo + grp, hi - 1)];
     for (int k0 = lo; k0 < hi; k0 += NPW) {
       const int k = k0 + grp;
       const bool valid = k < hi;
-      const int i = valid ? a.g.light[k] : a.g.light[lo];
-      const int64_t b = a.g.rowptr[i];
-      const int deg = valid ? static_cast<int>(a.g.rowptr[i + 1] - b) : 0;
+      const LightRow cur = nxt;
+      if (k0 + NPW < hi) nxt = LR[min(k + NPW, hi - 1)];
+      const int i = cur.row;
+      const int64_t b = cur.beg;
+      const int deg = valid ? cur.deg : 0;
       int dmax = deg;
 #pragma unroll
       for (int off = LPN; off < 64; off <<= 1) dmax = max(dmax, __shfl_xor(dmax, off));
@@ -496,11 +506,11 @@ __global__ __launch_bounds__(kBlock) void k_spmm(SpmmArgs a) {
         // a chunk with a long row: the whole wavefront takes its rows one at a time
         const int kn = min(NPW, hi - k0);
         for (int r = 0; r < kn; ++r) {
-          const int ir = a.g.light[k0 + r];
+          const LightRow lr = LR[k0 + r];
+          const int ir = lr.row;
           const V<T> pir = ldv(P + static_cast<int64_t>(ir) * KB + sub * VEC);
           V<T> accr = vzero<T>();
-          gather_row<T, LPN, W>(a.g.col, wgt, P, ir, a.g.rowptr[ir], a.g.rowptr[ir + 1], pir,
-                                accr, lane);
+          gather_row<T, LPN, W>(a.g.col, wgt, P, ir, lr.beg, lr.beg + lr.deg, pir, accr, lane);
           reduce_groups<T, LPN>(accr);
           if (lane < LPN) finish(ir, pir, accr, nullptr);
         }
