@@ -38,7 +38,13 @@ constexpr int kMaxSpmmGrid = 8192;
 constexpr int64_t kPiece = 1024;
 // Grid caps of the other kernels.
 constexpr int kMaxGridRhs = 8192;
-constexpr int kMaxGridUpd = 8192;
+// The update streams seven n x kb arrays; 32768 blocks (about 4.6 vectors per thread
+// and array on the 2.4M-node graph) ran it 5% faster than 8192 or 2048.  Its partial
+// sets then hold up to 32768 entries, which the finishing step folds into at most
+// 1024 level-1 sums (within kMaxTreeGrid).
+constexpr int kMaxGridUpd = 32768;
+static_assert((kMaxGridUpd + kTreeFan - 1) / kTreeFan <= kMaxTreeGrid,
+              "level-1 sums of the update partials must fit the tree buffers");
 constexpr int kMaxGridEd = 8192;
 constexpr int kCountBadGrid = kMaxTreeGrid;
 constexpr int kSampleGrid = 2048;
