@@ -75,8 +75,12 @@ Shape make_shape(int64_t n, int64_t nnz) {
   waves = std::min<int64_t>(waves, static_cast<int64_t>(kMaxSpmmGrid) * kWavesPerBlock);
   s.waves = static_cast<int>(waves);
   s.grid = s.waves / kWavesPerBlock;
-  s.heavy = std::max<int64_t>(256, static_cast<int64_t>(2.0 * s.share));
-  s.chunk = std::max<int64_t>(1024, static_cast<int64_t>(8.0 * s.share));
+  // Rows up to 1024 entries stay with the wavefronts (a block task costs a block-wide
+  // reduction), and a block task covers up to 4096 entries: on graphs with a small
+  // share (the 170k-node workload: 116 entries per wave) floors of 256 and 1024 made
+  // the SpMM 0.269 ms against 0.181 ms with these.
+  s.heavy = std::max<int64_t>(1024, static_cast<int64_t>(2.0 * s.share));
+  s.chunk = std::max<int64_t>(4096, static_cast<int64_t>(8.0 * s.share));
   s.ntask_max = nnz / s.heavy + nnz / s.chunk + 1;
   s.nmega_max = nnz / s.chunk + 1;
   s.nslot_max = 2 * (nnz / s.chunk) + 1;

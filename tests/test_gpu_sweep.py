@@ -1,6 +1,6 @@
 """Parity over a sweep of seeded graph shapes: power-law graphs whose rows reach every
 SpMM work path (rows gathered by a lane group, chunks gathered by the whole wavefront,
-block tasks above 256 entries, hub rows above 1024 entries split over several blocks),
+block tasks above 1024 entries, hub rows above 4096 entries split over several blocks),
 with isolated nodes and many components, weighted and unit, in both working
 precisions.  Every case checks the operator (L + delta I) X against the oracle within
 its rounding bound, and the whole path (resistance, curvature, sampling
@@ -16,13 +16,13 @@ from oracle import graph as OG
 
 torch = pytest.importorskip("torch")
 
-# name -> Chung-Lu arguments; (block tasks, multi-chunk rows, isolated nodes, components)
-# realised: cl6000: 17 rows > 256, 3 > 1024, 210 isolated; cl3000: 7 > 256, 177
-# isolated, 180 components; cl4097: largest component only (4066 nodes), 11 > 256;
-# cl1500: unit weights, 40 rows > 32; cl777: every row <= 32; cl65: one dense
-# component, every row between 12 and 54 entries
+# name -> Chung-Lu arguments; realised: cl10000: 6 rows > 1024 (block tasks), one of
+# 7554 entries > 4096 (split over two blocks), 394 isolated; cl3000: 7 rows > 256 (long
+# wavefront rows), 177 isolated, 180 components; cl4097: largest component only (4066
+# nodes), 11 rows > 256; cl1500: unit weights, 40 rows > 32; cl777: every row <= 32;
+# cl65: one dense component, every row between 12 and 54 entries
 SHAPES = {
-    "cl6000_g205": dict(n=6000, gamma=2.05, i0=0.3, m_target=30000, seed=16, weighted=True),
+    "cl10000_g20": dict(n=10000, gamma=2.0, i0=0.2, m_target=50000, seed=18, weighted=True),
     "cl3000_g21": dict(n=3000, gamma=2.1, i0=1.0, m_target=12000, seed=11, weighted=True),
     "cl4097_g23_lcc": dict(n=4097, gamma=2.3, i0=2.0, m_target=24000, seed=13, weighted=True,
                            keep_largest=True),
@@ -49,7 +49,8 @@ def _gpu():
 
 def test_sweep_shapes_reach_every_work_path():
     deg = {k: np.diff(_shape(k).rowptr) for k in SHAPES}
-    assert (deg["cl6000_g205"] > 1024).sum() >= 2
+    assert (deg["cl10000_g20"] > 4096).sum() >= 1
+    assert (deg["cl10000_g20"] > 1024).sum() >= 5
     assert (deg["cl3000_g21"] > 256).sum() >= 5
     assert any((d == 0).sum() > 100 for d in deg.values())
     assert any(((d > 32) & (d <= 256)).sum() > 10 for d in deg.values())
