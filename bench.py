@@ -32,9 +32,9 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 # the kernel source it was measured on: reported as null once that file changes.
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
-    "kernel_sha256_16": "90db047141efc012",
-    "fetch_bytes": 32598712307,
-    "write_bytes": 639565824,
+    "source_sha256_16": "b5e409821ef96926",
+    "fetch_bytes": 32491269134,
+    "write_bytes": 664731648,
     "profile": "profiles/k_spmm_cl2400k.md",
 }
 
@@ -52,11 +52,15 @@ def spmm_bytes_per_launch(g, kb: int, dtype: str) -> int:
 
 
 def kernel_source_hash() -> str:
+    """sha256 (first 16 hex digits) of the SpMM's kernel source and of the host code
+    that plans its launch; stored counter values are used only while both match."""
     import hashlib
 
-    path = os.path.join(ROOT, "paper_2609_27209_amd", "csrc", "erc_kernels.hip")
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in ("erc_kernels.hip", "erc_host.cpp"):
+        with open(os.path.join(ROOT, "paper_2609_27209_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def padded(kb: int, dtype: str) -> int:
@@ -388,7 +392,7 @@ def main() -> int:
     achieved = bytes_launch / (avg_spmm_ms / 1000.0) / 1e9
     traffic = None
     if (MEASURED_TRAFFIC["workload"] == args.config
-            and MEASURED_TRAFFIC["kernel_sha256_16"] == kernel_source_hash()):
+            and MEASURED_TRAFFIC["source_sha256_16"] == kernel_source_hash()):
         traffic = MEASURED_TRAFFIC["fetch_bytes"] + MEASURED_TRAFFIC["write_bytes"]
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
