@@ -120,6 +120,20 @@ def test_spmm_multichunk_rows():
     assert np.allclose(Yg, Yo, rtol=1e-12, atol=1e-9)
 
 
+def test_spmm_large_grid():
+    # 1.2M rows: more than 32 per wave at 8192 blocks, so the SpMM runs on a larger grid
+    E = _gpu()
+    n = 1_200_001
+    g = gen.path_graph(n, w=np.random.default_rng(5).uniform(0.5, 2.0, n - 1))
+    G = _graph(E, g, "f32")
+    X = np.random.default_rng(6).standard_normal((n, 16)).astype(np.float32)
+    Yg = G.debug_spmm(1e-3, torch.from_numpy(X)).cpu().numpy().astype(np.float64)
+    L = OG.laplacian(g)
+    Yo = OE.laplacian_apply(L, 1e-3, X.astype(np.float64))
+    scale = abs(L) @ np.abs(X.astype(np.float64)) + 1e-3 * np.abs(X)
+    assert np.all(np.abs(Yg - Yo) <= 4 * 2.0 ** -24 * 4 * scale + 1e-300)
+
+
 def _run_gpu(E, g, p):
     G = _graph(E, g, p.dtype)
     R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed)

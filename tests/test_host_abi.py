@@ -140,8 +140,10 @@ def test_work_plan_covers_every_entry(name):
 
 def test_work_plan_hub_and_isolated_cases():
     # a 20k-leaf star (a row split over several blocks), isolated nodes, a two-node graph
+    # ... and a 1.2M-node path, which has enough rows per wave for the larger SpMM grid
     for g in [gen.star_graph(20001), gen.from_edges(10, [0, 1], [1, 2]),
-              gen.from_edges(2, [0], [1]), gen.chung_lu(5000, 2.1, 3.0, 60000, seed=4)]:
+              gen.from_edges(2, [0], [1]), gen.chung_lu(5000, 2.1, 3.0, 60000, seed=4),
+              gen.path_graph(1_200_001)]:
         d, keep = _desc(g, "f64")
         _abi.erc_debug_check_plan(d)
 
