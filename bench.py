@@ -299,7 +299,7 @@ def block_sweep(name: str, widths):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="cl2400k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -372,9 +372,14 @@ def main() -> int:
     infos = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    step_ms = []
     for i in range(args.steps):
+        ts = time.perf_counter()
         infos.append(step(True))
-        log(f"step {i}: iters_max {infos[-1]['iters_max']} cg {infos[-1]['ms_cg']:.1f}ms")
+        torch.cuda.synchronize()  # a step is seconds long; this adds microseconds
+        step_ms.append((time.perf_counter() - ts) * 1000.0)
+        log(f"step {i}: {step_ms[-1]:.1f} ms, iters_max {infos[-1]['iters_max']} "
+            f"cg {infos[-1]['ms_cg']:.1f}ms")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1000.0 / args.steps
@@ -438,6 +443,8 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_median": round(sorted(step_ms)[len(step_ms) // 2], 2),
+        "step_ms": [round(t, 2) for t in step_ms],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -69,6 +69,7 @@ def test_bench_line(monkeypatch, capsys):
               "roofline", "cpu_baseline"):
         assert k in d, k
     assert (d["n_gpus"], d["steps"], d["warmup"]) == (1, 2, 1)
+    assert len(d["step_ms"]) == 2 and d["ms_per_step_median"] == max(d["step_ms"])
     assert d["higher_is_better"] is True and d["vs_baseline"] is None
     assert d["config"]["workload"] == "sbm20k" and d["dtype"] == "f32"
     g = gen.make_graph("sbm20k")
