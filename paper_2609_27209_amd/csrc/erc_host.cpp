@@ -38,6 +38,8 @@ constexpr double kRowCost = 8.0;
 constexpr int kBaseSpmmGrid = 8192;
 constexpr int kMaxSpmmGrid = 16384;
 constexpr int64_t kRowsPerWave = 32;
+static_assert((kMaxSpmmGrid + kTreeFan - 1) / kTreeFan <= kMaxTreeGrid,
+              "level-1 sums of the SpMM partials must fit the tree buffers");
 // Longest edge piece of the per-edge kernels.
 constexpr int64_t kPiece = 1024;
 // Grid caps of the other kernels.
