@@ -62,9 +62,17 @@ def draw(prob, draws: int, seed: int) -> np.ndarray:
     T = int(C[-1])
     if T == 0:
         raise ValueError("all weights are zero")
-    out = np.empty(draws, dtype=np.int64)
-    for d, t in enumerate(draw_targets(seed, T, draws)):
-        # the last i with C_i <= t; it has W_i > 0 because t < C_{i+1}
+    return select(C, draw_targets(seed, T, draws))
+
+
+def select(C, targets) -> np.ndarray:
+    """For each target t in [0, C[-1]), the item i with C[i] <= t < C[i+1], where C holds
+    the n+1 exclusive prefix sums of the integer weights (C[0] = 0).  Such an i has
+    W_i = C[i+1] - C[i] > 0, so items of weight zero are never selected."""
+    C = np.asarray(C, dtype=np.uint64)
+    out = np.empty(len(targets), dtype=np.int64)
+    for d, t in enumerate(targets):
+        # the last i with C_i <= t
         out[d] = int(np.searchsorted(C, np.uint64(t), side="right")) - 1
     return out
 

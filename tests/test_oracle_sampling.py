@@ -31,6 +31,16 @@ def test_targets_uniform_bits():
     assert t == [int(words[2 * d]) >> 44 for d in range(10)]
 
 
+def test_select_on_cdf_boundaries():
+    # W = [0, 3, 0, 5]: C = [0, 0, 3, 3, 8]; a target equal to C_i selects item i (the
+    # first with positive weight at that point), never a zero-weight item
+    C = np.array([0, 0, 3, 3, 8], dtype=np.uint64)
+    assert S.select(C, [0, 1, 2, 3, 4, 7]).tolist() == [1, 1, 1, 3, 3, 3]
+    # large weights near the top of the 64-bit range
+    big = np.array([0, 2**62, 2**62, 2**63 - 1], dtype=np.uint64)
+    assert S.select(big, [0, 2**62 - 1, 2**62, 2**63 - 2]).tolist() == [0, 0, 2, 2]
+
+
 def test_point_mass_and_zero_weights():
     assert set(S.draw([0.0, 1.0, 0.0], 200, 3)) == {1}
     d = S.draw([0.5, 0.0, 0.5, 0.0], 2000, 4)
