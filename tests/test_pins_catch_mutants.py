@@ -29,6 +29,7 @@ PINS_OF = {
     "exact.py": [os.path.join(_T, "test_oracle_exact.py")],
     "accurate.py": [os.path.join(_T, "test_oracle_accurate.py")],
     "sampling.py": [os.path.join(_T, "test_oracle_sampling.py")],
+    "agreement.py": [os.path.join(_T, "test_oracle_agreement.py")],
 }
 
 # (id, module, original text, planted text); the first occurrence is changed, which for
@@ -45,6 +46,14 @@ MUTANTS = [
     ("cg_residual_sign", "erc.py", "Ra = R[:, a] - alpha * Qa", "Ra = R[:, a] + alpha * Qa"),
     ("cg_iterate_not_updated", "erc.py", "Z[:, a] += alpha * Pa", "Z[:, a] += Pa"),
     ("cg_stop_tol_not_squared", "erc.py", "thr = tol * tol * rho0", "thr = tol * rho0"),
+    # the Jacobi-preconditioned variant
+    ("pcg_direction_unpreconditioned", "erc.py",
+     "P[:, a[keep]] = Sa[:, keep] + beta[keep] * Pa[:, keep]",
+     "P[:, a[keep]] = Ra[:, keep] + beta[keep] * Pa[:, keep]"),
+    ("pcg_rho_r_dot_r", "erc.py", "rho_new = dot2_columns(Ra, Sa)", "rho_new = dot2_columns(Ra, Ra)"),
+    ("pcg_diagonal_without_shift", "erc.py",
+     "return 1.0 / (np.asarray(L.diagonal(), dtype=np.float64) + delta)",
+     "return 1.0 / np.asarray(L.diagonal(), dtype=np.float64)"),
     # R_e = ||Z_u - Z_v||^2 (Eq. 6)
     ("distance_not_squared", "erc.py", 'np.einsum("ij,ij->i", d, d)',
      'np.sqrt(np.einsum("ij,ij->i", d, d))'),
@@ -81,6 +90,11 @@ MUTANTS = [
      "return Lp[eu, eu] + Lp[ev, ev] + 2.0 * Lp[eu, ev]"),
     # compensated dot products
     ("two_sum_error_term", "accurate.py", "e = (a - (s - z)) + (b - z)", "e = (a - (s - z)) - (b - z)"),
+    # Table 2 metrics
+    ("rank_ties_not_averaged", "agreement.py", "ranks[order[i:j + 1]] = 0.5 * (i + j) + 1.0",
+     "ranks[order[i:j + 1]] = i + 1.0"),
+    ("mae_signed", "agreement.py", "return float(np.mean(np.abs(a - b)))",
+     "return float(np.abs(np.mean(a - b)))"),
     # curvature-guided draws
     ("draw_search_boundary", "sampling.py", 'side="right")) - 1', 'side="left")) - 1'),
     ("draw_scale_bits", "sampling.py", "SCALE_BITS = 62", "SCALE_BITS = 61"),
