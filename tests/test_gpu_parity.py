@@ -255,6 +255,24 @@ def test_solve_block_matches_oracle_cg():
     assert np.allclose(Zg, res.Z, rtol=1e-9, atol=1e-9 * np.abs(res.Z).max())
 
 
+def test_large_grid_solve_matches_oracle_and_repeats():
+    # 1.2M rows (the larger SpMM grid): one column of RHS + fp64 CG against the oracle
+    # (same iteration count, Z to 1e-9), and two runs bit-identical
+    E = _gpu()
+    n = 1_200_001
+    g = gen.path_graph(n, w=np.random.default_rng(5).uniform(0.5, 2.0, n - 1))
+    G = _graph(E, g, "f64")
+    K, delta, tol, seed = 16, 1.0, 1e-10, 9
+    Z1, it1, _ = G.debug_solve_block(K, 8, delta, tol, seed, 0, 1)
+    Z2, it2, _ = G.debug_solve_block(K, 8, delta, tol, seed, 0, 1)
+    Z1 = Z1.cpu().numpy()
+    assert np.array_equal(Z1, Z2.cpu().numpy()) and list(it1) == list(it2)
+    Y = OE.rhs(g, K, 0, 1, seed, "f64")
+    res = OE.cg_columns(OG.laplacian(g), delta, Y, tol, 1000)
+    assert np.array_equal(np.array(it1), res.iters)
+    assert np.allclose(Z1, res.Z, rtol=1e-9, atol=1e-9 * np.abs(res.Z).max())
+
+
 def test_invalid_arguments_raise():
     E = _gpu()
     g = gen.make_graph("er2k")
