@@ -32,7 +32,7 @@ PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 # the kernel source it was measured on: reported as null once that file changes.
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
-    "source_sha256_16": "10a511770d27cda1",
+    "source_sha256_16": "d0cf3eae15d6ac09",
     "fetch_bytes": 32491269134,
     "write_bytes": 664731648,
     "profile": "profiles/k_spmm_cl2400k.md",

@@ -14,7 +14,8 @@
  *   5. node / edge sampling probabilities                (Eqs. 7, 8; Section 3.2)
  *
  * Conventions shared by every call
- *  - Every function returns an erc_status; nothing is thrown across the ABI.  On an
+ *  - Every function returns an erc_status; nothing is thrown across the ABI (host-side
+ *    failures such as an allocation that cannot be served become ERC_E_HOST).  On an
  *    error, erc_last_error() returns a message (thread-local, valid until the next
  *    call on the same thread).
  *  - "host" pointers are ordinary CPU memory; "device" pointers are GPU memory on the
@@ -48,7 +49,8 @@ typedef enum {
   ERC_E_DEVICE = 4,          /* a HIP runtime call failed                              */
   ERC_E_NOT_CONVERGED = 5,   /* some column hit max_iter above tol (result written)    */
   ERC_E_NUMERIC = 6,         /* CG breakdown (p.q <= 0 or non-finite), R <= 0, NaN     */
-  ERC_E_STATE = 7            /* handle used in an invalid state                        */
+  ERC_E_STATE = 7,           /* handle used in an invalid state                        */
+  ERC_E_HOST = 8             /* host memory could not be allocated or a thread started */
 } erc_status;
 
 typedef enum { ERC_F32 = 0, ERC_F64 = 1 } erc_dtype;

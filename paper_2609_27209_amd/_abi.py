@@ -21,6 +21,7 @@ ERC_E_DEVICE = 4
 ERC_E_NOT_CONVERGED = 5
 ERC_E_NUMERIC = 6
 ERC_E_STATE = 7
+ERC_E_HOST = 8
 
 ERC_F32 = 0
 ERC_F64 = 1
@@ -67,7 +68,8 @@ class ErcNotConverged(ErcError):
 
 
 _NAMES = {0: "ERC_OK", 1: "ERC_E_INVALID_ARG", 2: "ERC_E_INVALID_GRAPH", 3: "ERC_E_WORKSPACE",
-          4: "ERC_E_DEVICE", 5: "ERC_E_NOT_CONVERGED", 6: "ERC_E_NUMERIC", 7: "ERC_E_STATE"}
+          4: "ERC_E_DEVICE", 5: "ERC_E_NOT_CONVERGED", 6: "ERC_E_NUMERIC", 7: "ERC_E_STATE",
+          8: "ERC_E_HOST"}
 
 
 def _status_name(s: int) -> str:

@@ -4,10 +4,15 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <climits>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
+#include <exception>
+#include <new>
 #include <numeric>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "erc_common.h"
@@ -21,6 +26,21 @@ thread_local std::string g_last_error;
 erc_status fail(erc_status s, const std::string& msg) {
   g_last_error = msg;
   return s;
+}
+
+// The C ABI throws nothing: a failed host allocation or thread start inside a call
+// becomes ERC_E_HOST with a message.
+template <typename F>
+erc_status guarded(F&& f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    return fail(ERC_E_HOST, "host memory allocation failed");
+  } catch (const std::exception& e) {
+    return fail(ERC_E_HOST, std::string("host error: ") + e.what());
+  } catch (...) {
+    return fail(ERC_E_HOST, "host error");
+  }
 }
 
 #define ERC_HIP(call)                                                                  \
@@ -160,6 +180,59 @@ struct Canon {
   std::vector<unsigned char> wstore;  // nnz weights in the working precision
 };
 
+// Rows [0, n) split into `parts` contiguous ranges of about equal stored entries, each
+// handled by its own thread (one thread for small graphs).
+template <typename F>
+void for_row_ranges(const int64_t* rp, int64_t n, F&& body) {
+  const int64_t nnz = rp[n];
+  int parts = 1;
+  if (nnz >= (int64_t(1) << 20)) {
+    const unsigned hc = std::thread::hardware_concurrency();
+    parts = static_cast<int>(std::min<unsigned>(hc == 0 ? 1u : hc, 16u));
+  }
+  std::vector<int64_t> cut(parts + 1, n);
+  cut[0] = 0;
+  for (int t = 1; t < parts; ++t)
+    cut[t] = std::upper_bound(rp, rp + n + 1, nnz * t / parts) - rp - 1;
+  for (int t = 1; t <= parts; ++t) cut[t] = std::max(cut[t], cut[t - 1]);
+  if (parts == 1) {
+    body(0, int64_t(0), n);
+    return;
+  }
+  // an exception in a worker (a failed allocation) is rethrown here, after all joined
+  std::vector<std::exception_ptr> exc(parts);
+  std::vector<std::thread> th;
+  auto run = [&](int t) {
+    try {
+      body(t, cut[t], cut[t + 1]);
+    } catch (...) {
+      exc[t] = std::current_exception();
+    }
+  };
+  try {
+    for (int t = 0; t < parts; ++t) th.emplace_back(run, t);
+  } catch (...) {
+    for (auto& x : th) x.join();
+    throw;
+  }
+  for (auto& x : th) x.join();
+  for (auto& e : exc)
+    if (e) std::rethrow_exception(e);
+}
+
+// The first problem a worker finds in its row range; the caller reports the one in
+// the lowest row (workers never touch the thread-local error message).
+struct RowError {
+  int64_t row = INT64_MAX;
+  std::string msg;
+  void set(int64_t r, std::string m) {
+    if (r < row) {
+      row = r;
+      msg = std::move(m);
+    }
+  }
+};
+
 template <typename WT>
 erc_status sweep(const erc_graph_desc* d, const WT* w, Canon* out) {
   const int64_t n = d->n;
@@ -169,54 +242,102 @@ erc_status sweep(const erc_graph_desc* d, const WT* w, Canon* out) {
   for (int64_t i = 0; i < n; ++i)
     if (rp[i + 1] < rp[i]) return fail(ERC_E_INVALID_GRAPH, "rowptr decreases at row " + std::to_string(i));
   if (nnz % 2 != 0) return fail(ERC_E_INVALID_GRAPH, "odd number of stored entries: not symmetric");
-  std::vector<int64_t> cursor(n, 0);
   if (out) {
     out->eid.assign(nnz, -1);
-    out->sw.assign(nnz / 2, 0.0);
     out->ubase.assign(n + 1, 0);
     out->deg.assign(n, 0.0);
   }
-  int64_t next_edge = 0;
-  for (int64_t i = 0; i < n; ++i) {
-    if (out) out->ubase[i] = next_edge;
-    for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) {
-      const int64_t j = col[pos];
-      if (j < 0 || j >= n)
-        return fail(ERC_E_INVALID_GRAPH, "column index out of range in row " + std::to_string(i));
-      if (j == i) return fail(ERC_E_INVALID_GRAPH, "self-loop at node " + std::to_string(i));
-      if (pos > rp[i] && col[pos - 1] >= j)
-        return fail(ERC_E_INVALID_GRAPH,
-                    "columns not strictly ascending in row " + std::to_string(i));
-      // the i-th node to list j must be j's next stored neighbour
-      const int64_t tpos = rp[j] + cursor[j]++;
-      if (tpos >= rp[j + 1] || col[tpos] != i)
-        return fail(ERC_E_INVALID_GRAPH, "structure is not symmetric at entry (" +
-                                             std::to_string(i) + ", " + std::to_string(j) + ")");
-      if (w != nullptr) {
-        const WT x = w[pos];
-        if (!(std::isfinite(static_cast<double>(x)) && x > WT(0)))
-          return fail(ERC_E_INVALID_GRAPH, "weight must be finite and > 0 at entry (" +
-                                               std::to_string(i) + ", " + std::to_string(j) + ")");
-        if (!(w[tpos] == x))
-          return fail(ERC_E_INVALID_GRAPH, "weights not symmetric at entry (" +
-                                               std::to_string(i) + ", " + std::to_string(j) + ")");
-      }
-      if (out) out->deg[i] += (w != nullptr) ? static_cast<double>(w[pos]) : 1.0;
-      if (i < j) {
-        if (out) {
-          out->eid[pos] = static_cast<int32_t>(next_edge);
-          out->eid[tpos] = static_cast<int32_t>(next_edge);
-          out->sw[next_edge] = (w != nullptr) ? std::sqrt(static_cast<double>(w[pos])) : 1.0;
+  // 1. per row: indices in range, no self-loop, strictly ascending, weights finite and
+  //    positive; the number of upper entries (j > i) and d_i in CSR order
+  std::vector<int64_t> nup(n, 0);
+  std::vector<RowError> err1(16);
+  for_row_ranges(rp, n, [&](int t, int64_t r0, int64_t r1) {
+    RowError& e = err1[t];
+    for (int64_t i = r0; i < r1 && e.row == INT64_MAX; ++i) {
+      int64_t up = 0;
+      double dsum = 0.0;
+      for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) {
+        const int64_t j = col[pos];
+        if (j < 0 || j >= n) {
+          e.set(i, "column index out of range in row " + std::to_string(i));
+          break;
         }
-        ++next_edge;
+        if (j == i) {
+          e.set(i, "self-loop at node " + std::to_string(i));
+          break;
+        }
+        if (pos > rp[i] && col[pos - 1] >= j) {
+          e.set(i, "columns not strictly ascending in row " + std::to_string(i));
+          break;
+        }
+        if (w != nullptr) {
+          const WT x = w[pos];
+          if (!(std::isfinite(static_cast<double>(x)) && x > WT(0))) {
+            e.set(i, "weight must be finite and > 0 at entry (" + std::to_string(i) + ", " +
+                         std::to_string(j) + ")");
+            break;
+          }
+        }
+        dsum += (w != nullptr) ? static_cast<double>(w[pos]) : 1.0;
+        up += (j > i) ? 1 : 0;
+      }
+      nup[i] = up;
+      if (out) out->deg[i] = dsum;
+    }
+  });
+  {
+    RowError first;
+    for (const RowError& e : err1) first.set(e.row, e.msg);
+    if (first.row != INT64_MAX) return fail(ERC_E_INVALID_GRAPH, first.msg);
+  }
+  // 2. canonical edge ids: the upper entries in row-major order
+  std::vector<int64_t> ub(n + 1, 0);
+  for (int64_t i = 0; i < n; ++i) ub[i + 1] = ub[i] + nup[i];
+  const int64_t m = ub[n];
+  if (m * 2 != nnz) return fail(ERC_E_INVALID_GRAPH, "structure is not symmetric");
+  if (out) {
+    std::copy(ub.begin(), ub.end(), out->ubase.begin());
+    out->sw.assign(m, 0.0);
+  }
+  // 3. every upper entry (i, j) has its mirror (j, i) with the same weight; as there are
+  //    as many lower entries as upper ones, the mirrors are all of them.  Each edge id
+  //    slot is written once, by the thread of the upper entry's row.
+  std::vector<RowError> err3(16);
+  for_row_ranges(rp, n, [&](int t, int64_t r0, int64_t r1) {
+    RowError& e = err3[t];
+    for (int64_t i = r0; i < r1 && e.row == INT64_MAX; ++i) {
+      const int64_t first_up = rp[i + 1] - nup[i];
+      for (int64_t pos = first_up; pos < rp[i + 1]; ++pos) {
+        const int64_t j = col[pos];
+        const int32_t* lo = col + rp[j];
+        const int32_t* hi = col + rp[j + 1];
+        const int32_t* it = std::lower_bound(lo, hi, static_cast<int32_t>(i));
+        if (it == hi || *it != i) {
+          e.set(i, "structure is not symmetric at entry (" + std::to_string(i) + ", " +
+                       std::to_string(j) + ")");
+          break;
+        }
+        const int64_t tpos = it - col;
+        if (w != nullptr && !(w[tpos] == w[pos])) {
+          e.set(i, "weights not symmetric at entry (" + std::to_string(i) + ", " +
+                       std::to_string(j) + ")");
+          break;
+        }
+        if (out) {
+          const int64_t id = ub[i] + (pos - first_up);
+          out->eid[pos] = static_cast<int32_t>(id);
+          out->eid[tpos] = static_cast<int32_t>(id);
+          out->sw[id] = (w != nullptr) ? std::sqrt(static_cast<double>(w[pos])) : 1.0;
+        }
       }
     }
+  });
+  {
+    RowError first;
+    for (const RowError& e : err3) first.set(e.row, e.msg);
+    if (first.row != INT64_MAX) return fail(ERC_E_INVALID_GRAPH, first.msg);
   }
-  if (out) {
-    out->ubase[n] = next_edge;
-    out->m = next_edge;
-  }
-  if (next_edge * 2 != nnz) return fail(ERC_E_INVALID_GRAPH, "structure is not symmetric");
+  if (out) out->m = m;
   return ERC_OK;
 }
 
@@ -630,6 +751,7 @@ const char* erc_status_string(erc_status s) {
     case ERC_E_NOT_CONVERGED: return "not converged";
     case ERC_E_NUMERIC: return "numerical breakdown";
     case ERC_E_STATE: return "invalid state";
+    case ERC_E_HOST: return "host allocation or thread failure";
   }
   return "unknown status";
 }
@@ -637,318 +759,338 @@ const char* erc_status_string(erc_status s) {
 const char* erc_last_error(void) { return g_last_error.c_str(); }
 
 erc_status erc_validate(const erc_graph_desc* desc, int64_t* m_out) {
-  g_last_error.clear();
-  erc_status st = check_desc(desc);
-  if (st != ERC_OK) return st;
-  Canon c;
-  if (desc->w == nullptr) st = sweep<float>(desc, nullptr, nullptr);
-  else if (desc->w_dtype == ERC_F32) st = sweep<float>(desc, static_cast<const float*>(desc->w), nullptr);
-  else st = sweep<double>(desc, static_cast<const double*>(desc->w), nullptr);
-  if (st != ERC_OK) return st;
-  if (m_out) *m_out = desc->rowptr[desc->n] / 2;
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    erc_status st = check_desc(desc);
+    if (st != ERC_OK) return st;
+    Canon c;
+    if (desc->w == nullptr) st = sweep<float>(desc, nullptr, nullptr);
+    else if (desc->w_dtype == ERC_F32) st = sweep<float>(desc, static_cast<const float*>(desc->w), nullptr);
+    else st = sweep<double>(desc, static_cast<const double*>(desc->w), nullptr);
+    if (st != ERC_OK) return st;
+    if (m_out) *m_out = desc->rowptr[desc->n] / 2;
+    return ERC_OK;
+  });
 }
 
 erc_status erc_graph_bytes(const erc_graph_desc* desc, size_t* bytes) {
-  g_last_error.clear();
-  erc_status st = check_desc(desc);
-  if (st != ERC_OK) return st;
-  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
-  const Shape s = make_shape(desc->n, desc->rowptr[desc->n]);
-  *bytes = static_cast<size_t>(graph_layout(s, desc->w != nullptr, desc->solve_dtype).total);
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    erc_status st = check_desc(desc);
+    if (st != ERC_OK) return st;
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    const Shape s = make_shape(desc->n, desc->rowptr[desc->n]);
+    *bytes = static_cast<size_t>(graph_layout(s, desc->w != nullptr, desc->solve_dtype).total);
+    return ERC_OK;
+  });
 }
 
 erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, void* stream,
                       erc_handle* out) {
-  g_last_error.clear();
-  if (out == nullptr) return fail(ERC_E_INVALID_ARG, "out is NULL");
-  *out = nullptr;
-  if (dev_mem == nullptr) return fail(ERC_E_INVALID_ARG, "dev_mem is NULL");
-  if (reinterpret_cast<uintptr_t>(dev_mem) % 256 != 0)
-    return fail(ERC_E_INVALID_ARG, "dev_mem must be 256-byte aligned");
-  Canon c;
-  erc_status st = canonicalise(desc, &c);
-  if (st != ERC_OK) return st;
-  const int64_t n = desc->n;
-  const int64_t nnz = desc->rowptr[n];
-  const Shape s = make_shape(n, nnz);
-  const bool weighted = desc->w != nullptr;
-  const GraphLayout L = graph_layout(s, weighted, desc->solve_dtype);
-  if (static_cast<int64_t>(bytes) < L.total)
-    return fail(ERC_E_WORKSPACE, "graph buffer smaller than erc_graph_bytes");
-  Plan P;
-  build_plan(desc, c, s, &P);
-  if (static_cast<int64_t>(P.task_row.size()) > s.ntask_max ||
-      static_cast<int64_t>(P.mega_nchunk.size()) > s.nmega_max ||
-      static_cast<int64_t>(P.piece_row.size()) > s.npiece_max || P.nslot > s.nslot_max)
-    return fail(ERC_E_STATE, "internal: work plan exceeds its size bound");
-  // weights in the working precision
-  std::vector<float> wf;
-  std::vector<double> wd;
-  const void* wsrc = nullptr;
-  if (weighted) {
-    if (desc->solve_dtype == ERC_F32) {
-      if (desc->w_dtype == ERC_F32) {
-        wsrc = desc->w;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (out == nullptr) return fail(ERC_E_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (dev_mem == nullptr) return fail(ERC_E_INVALID_ARG, "dev_mem is NULL");
+    if (reinterpret_cast<uintptr_t>(dev_mem) % 256 != 0)
+      return fail(ERC_E_INVALID_ARG, "dev_mem must be 256-byte aligned");
+    Canon c;
+    erc_status st = canonicalise(desc, &c);
+    if (st != ERC_OK) return st;
+    const int64_t n = desc->n;
+    const int64_t nnz = desc->rowptr[n];
+    const Shape s = make_shape(n, nnz);
+    const bool weighted = desc->w != nullptr;
+    const GraphLayout L = graph_layout(s, weighted, desc->solve_dtype);
+    if (static_cast<int64_t>(bytes) < L.total)
+      return fail(ERC_E_WORKSPACE, "graph buffer smaller than erc_graph_bytes");
+    Plan P;
+    build_plan(desc, c, s, &P);
+    if (static_cast<int64_t>(P.task_row.size()) > s.ntask_max ||
+        static_cast<int64_t>(P.mega_nchunk.size()) > s.nmega_max ||
+        static_cast<int64_t>(P.piece_row.size()) > s.npiece_max || P.nslot > s.nslot_max)
+      return fail(ERC_E_STATE, "internal: work plan exceeds its size bound");
+    // weights in the working precision
+    std::vector<float> wf;
+    std::vector<double> wd;
+    const void* wsrc = nullptr;
+    if (weighted) {
+      if (desc->solve_dtype == ERC_F32) {
+        if (desc->w_dtype == ERC_F32) {
+          wsrc = desc->w;
+        } else {
+          wf.resize(nnz);
+          const double* x = static_cast<const double*>(desc->w);
+          for (int64_t k = 0; k < nnz; ++k) wf[k] = static_cast<float>(x[k]);
+          wsrc = wf.data();
+        }
       } else {
-        wf.resize(nnz);
-        const double* x = static_cast<const double*>(desc->w);
-        for (int64_t k = 0; k < nnz; ++k) wf[k] = static_cast<float>(x[k]);
-        wsrc = wf.data();
-      }
-    } else {
-      if (desc->w_dtype == ERC_F64) {
-        wsrc = desc->w;
-      } else {
-        wd.resize(nnz);
-        const float* x = static_cast<const float*>(desc->w);
-        for (int64_t k = 0; k < nnz; ++k) wd[k] = static_cast<double>(x[k]);
-        wsrc = wd.data();
+        if (desc->w_dtype == ERC_F64) {
+          wsrc = desc->w;
+        } else {
+          wd.resize(nnz);
+          const float* x = static_cast<const float*>(desc->w);
+          for (int64_t k = 0; k < nnz; ++k) wd[k] = static_cast<double>(x[k]);
+          wsrc = wd.data();
+        }
       }
     }
-  }
-  auto* h = new erc_graph_s();
-  h->n = n;
-  h->nnz = nnz;
-  h->m = c.m;
-  h->dt = desc->solve_dtype;
-  h->weighted = weighted;
-  h->shape = s;
-  for (int64_t i = 0; i < n; ++i) h->nonisolated += desc->rowptr[i + 1] > desc->rowptr[i];
-  auto cleanup = [&](erc_status e) {
-    if (h->pinned) (void)hipHostFree(h->pinned);
+    auto* h = new erc_graph_s();
+    h->n = n;
+    h->nnz = nnz;
+    h->m = c.m;
+    h->dt = desc->solve_dtype;
+    h->weighted = weighted;
+    h->shape = s;
+    for (int64_t i = 0; i < n; ++i) h->nonisolated += desc->rowptr[i + 1] > desc->rowptr[i];
+    auto cleanup = [&](erc_status e) {
+      if (h->pinned) (void)hipHostFree(h->pinned);
+      for (auto& ev : h->ev)
+        if (ev) (void)hipEventDestroy(ev);
+      delete h;
+      return e;
+    };
+    if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipGetDevice failed"));
+    if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), kPinnedInts * sizeof(int32_t),
+                      hipHostMallocDefault) != hipSuccess)
+      return cleanup(fail(ERC_E_DEVICE, "hipHostMalloc failed"));
     for (auto& ev : h->ev)
-      if (ev) (void)hipEventDestroy(ev);
-    delete h;
-    return e;
-  };
-  if (hipGetDevice(&h->device) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipGetDevice failed"));
-  if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), kPinnedInts * sizeof(int32_t),
-                    hipHostMallocDefault) != hipSuccess)
-    return cleanup(fail(ERC_E_DEVICE, "hipHostMalloc failed"));
-  for (auto& ev : h->ev)
-    if (hipEventCreate(&ev) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipEventCreate failed"));
-  char* base = static_cast<char*>(dev_mem);
-  hipStream_t hs = static_cast<hipStream_t>(stream);
-  auto up = [&](int64_t off, const void* src, int64_t nbytes) -> hipError_t {
-    if (nbytes <= 0) return hipSuccess;
-    return hipMemcpyAsync(base + off, src, nbytes, hipMemcpyHostToDevice, hs);
-  };
-  hipError_t e = hipSuccess;
-  auto chk = [&](hipError_t x) { if (e == hipSuccess) e = x; };
-  chk(up(L.rowptr, desc->rowptr, (n + 1) * 8));
-  chk(up(L.col, desc->col, nnz * 4));
-  if (weighted) chk(up(L.w, wsrc, nnz * static_cast<int64_t>(dsize(desc->solve_dtype))));
-  chk(up(L.eid, c.eid.data(), nnz * 4));
-  chk(up(L.sw, c.sw.data(), c.m * 8));
-  chk(up(L.ubase, c.ubase.data(), (n + 1) * 8));
-  chk(up(L.deg, c.deg.data(), n * 8));
-  std::vector<LightRow> lrows(P.light.size());
-  for (size_t k = 0; k < P.light.size(); ++k) {
-    const int32_t i = P.light[k];
-    lrows[k] = LightRow{desc->rowptr[i], i, static_cast<int32_t>(desc->rowptr[i + 1] - desc->rowptr[i])};
-  }
-  chk(up(L.light, lrows.data(), static_cast<int64_t>(lrows.size() * sizeof(LightRow))));
-  chk(up(L.wave_lo, P.wave_lo.data(), static_cast<int64_t>(P.wave_lo.size()) * 4));
-  const int64_t nt = static_cast<int64_t>(P.task_row.size());
-  chk(up(L.task_row, P.task_row.data(), nt * 4));
-  chk(up(L.task_mega, P.task_mega.data(), nt * 4));
-  chk(up(L.task_chunk, P.task_chunk.data(), nt * 4));
-  chk(up(L.task_beg, P.task_beg.data(), nt * 8));
-  chk(up(L.task_end, P.task_end.data(), nt * 8));
-  const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
-  chk(up(L.mega_nchunk, P.mega_nchunk.data(), nm * 4));
-  chk(up(L.mega_chunk0, P.mega_chunk0.data(), nm * 4));
-  const int64_t np = static_cast<int64_t>(P.piece_row.size());
-  chk(up(L.piece_row, P.piece_row.data(), np * 4));
-  chk(up(L.piece_beg, P.piece_beg.data(), np * 8));
-  chk(up(L.piece_end, P.piece_end.data(), np * 8));
-  if (e == hipSuccess) e = hipStreamSynchronize(hs);
-  if (e != hipSuccess) return cleanup(fail(ERC_E_DEVICE, std::string("graph upload: ") + hipGetErrorString(e)));
-  DevGraph& g = h->dg;
-  g.n = static_cast<int32_t>(n);
-  g.nnz = nnz;
-  g.m = c.m;
-  g.weighted = weighted ? 1 : 0;
-  // the stored weights equal the input ones unless fp64 input is rounded to fp32
-  g.sw_from_w = (weighted && !(desc->w_dtype == ERC_F64 && desc->solve_dtype == ERC_F32)) ? 1 : 0;
-  g.rowptr = reinterpret_cast<const int64_t*>(base + L.rowptr);
-  g.col = reinterpret_cast<const int32_t*>(base + L.col);
-  g.w = weighted ? base + L.w : nullptr;
-  g.eid = reinterpret_cast<const int32_t*>(base + L.eid);
-  g.sw = reinterpret_cast<const double*>(base + L.sw);
-  g.ubase = reinterpret_cast<const int64_t*>(base + L.ubase);
-  g.deg = reinterpret_cast<const double*>(base + L.deg);
-  g.grid = s.grid;
-  g.light = reinterpret_cast<const LightRow*>(base + L.light);
-  g.wave_lo = reinterpret_cast<const int32_t*>(base + L.wave_lo);
-  g.ntask = static_cast<int32_t>(nt);
-  g.task_row = reinterpret_cast<const int32_t*>(base + L.task_row);
-  g.task_mega = reinterpret_cast<const int32_t*>(base + L.task_mega);
-  g.task_chunk = reinterpret_cast<const int32_t*>(base + L.task_chunk);
-  g.task_beg = reinterpret_cast<const int64_t*>(base + L.task_beg);
-  g.task_end = reinterpret_cast<const int64_t*>(base + L.task_end);
-  g.nmega = static_cast<int32_t>(nm);
-  g.mega_nchunk = reinterpret_cast<const int32_t*>(base + L.mega_nchunk);
-  g.mega_chunk0 = reinterpret_cast<const int32_t*>(base + L.mega_chunk0);
-  g.nchunk_slots = P.nslot;
-  g.npiece = np;
-  g.piece_row = reinterpret_cast<const int32_t*>(base + L.piece_row);
-  g.piece_beg = reinterpret_cast<const int64_t*>(base + L.piece_beg);
-  g.piece_end = reinterpret_cast<const int64_t*>(base + L.piece_end);
-  *out = h;
-  return ERC_OK;
+      if (hipEventCreate(&ev) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipEventCreate failed"));
+    char* base = static_cast<char*>(dev_mem);
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    auto up = [&](int64_t off, const void* src, int64_t nbytes) -> hipError_t {
+      if (nbytes <= 0) return hipSuccess;
+      return hipMemcpyAsync(base + off, src, nbytes, hipMemcpyHostToDevice, hs);
+    };
+    hipError_t e = hipSuccess;
+    auto chk = [&](hipError_t x) { if (e == hipSuccess) e = x; };
+    chk(up(L.rowptr, desc->rowptr, (n + 1) * 8));
+    chk(up(L.col, desc->col, nnz * 4));
+    if (weighted) chk(up(L.w, wsrc, nnz * static_cast<int64_t>(dsize(desc->solve_dtype))));
+    chk(up(L.eid, c.eid.data(), nnz * 4));
+    chk(up(L.sw, c.sw.data(), c.m * 8));
+    chk(up(L.ubase, c.ubase.data(), (n + 1) * 8));
+    chk(up(L.deg, c.deg.data(), n * 8));
+    std::vector<LightRow> lrows(P.light.size());
+    for (size_t k = 0; k < P.light.size(); ++k) {
+      const int32_t i = P.light[k];
+      lrows[k] = LightRow{desc->rowptr[i], i, static_cast<int32_t>(desc->rowptr[i + 1] - desc->rowptr[i])};
+    }
+    chk(up(L.light, lrows.data(), static_cast<int64_t>(lrows.size() * sizeof(LightRow))));
+    chk(up(L.wave_lo, P.wave_lo.data(), static_cast<int64_t>(P.wave_lo.size()) * 4));
+    const int64_t nt = static_cast<int64_t>(P.task_row.size());
+    chk(up(L.task_row, P.task_row.data(), nt * 4));
+    chk(up(L.task_mega, P.task_mega.data(), nt * 4));
+    chk(up(L.task_chunk, P.task_chunk.data(), nt * 4));
+    chk(up(L.task_beg, P.task_beg.data(), nt * 8));
+    chk(up(L.task_end, P.task_end.data(), nt * 8));
+    const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
+    chk(up(L.mega_nchunk, P.mega_nchunk.data(), nm * 4));
+    chk(up(L.mega_chunk0, P.mega_chunk0.data(), nm * 4));
+    const int64_t np = static_cast<int64_t>(P.piece_row.size());
+    chk(up(L.piece_row, P.piece_row.data(), np * 4));
+    chk(up(L.piece_beg, P.piece_beg.data(), np * 8));
+    chk(up(L.piece_end, P.piece_end.data(), np * 8));
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return cleanup(fail(ERC_E_DEVICE, std::string("graph upload: ") + hipGetErrorString(e)));
+    DevGraph& g = h->dg;
+    g.n = static_cast<int32_t>(n);
+    g.nnz = nnz;
+    g.m = c.m;
+    g.weighted = weighted ? 1 : 0;
+    // the stored weights equal the input ones unless fp64 input is rounded to fp32
+    g.sw_from_w = (weighted && !(desc->w_dtype == ERC_F64 && desc->solve_dtype == ERC_F32)) ? 1 : 0;
+    g.rowptr = reinterpret_cast<const int64_t*>(base + L.rowptr);
+    g.col = reinterpret_cast<const int32_t*>(base + L.col);
+    g.w = weighted ? base + L.w : nullptr;
+    g.eid = reinterpret_cast<const int32_t*>(base + L.eid);
+    g.sw = reinterpret_cast<const double*>(base + L.sw);
+    g.ubase = reinterpret_cast<const int64_t*>(base + L.ubase);
+    g.deg = reinterpret_cast<const double*>(base + L.deg);
+    g.grid = s.grid;
+    g.light = reinterpret_cast<const LightRow*>(base + L.light);
+    g.wave_lo = reinterpret_cast<const int32_t*>(base + L.wave_lo);
+    g.ntask = static_cast<int32_t>(nt);
+    g.task_row = reinterpret_cast<const int32_t*>(base + L.task_row);
+    g.task_mega = reinterpret_cast<const int32_t*>(base + L.task_mega);
+    g.task_chunk = reinterpret_cast<const int32_t*>(base + L.task_chunk);
+    g.task_beg = reinterpret_cast<const int64_t*>(base + L.task_beg);
+    g.task_end = reinterpret_cast<const int64_t*>(base + L.task_end);
+    g.nmega = static_cast<int32_t>(nm);
+    g.mega_nchunk = reinterpret_cast<const int32_t*>(base + L.mega_nchunk);
+    g.mega_chunk0 = reinterpret_cast<const int32_t*>(base + L.mega_chunk0);
+    g.nchunk_slots = P.nslot;
+    g.npiece = np;
+    g.piece_row = reinterpret_cast<const int32_t*>(base + L.piece_row);
+    g.piece_beg = reinterpret_cast<const int64_t*>(base + L.piece_beg);
+    g.piece_end = reinterpret_cast<const int64_t*>(base + L.piece_end);
+    *out = h;
+    return ERC_OK;
+  });
 }
 
 erc_status erc_num_nodes(erc_handle h, int64_t* n) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (n == nullptr) return fail(ERC_E_INVALID_ARG, "n is NULL");
-  *n = h->n;
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (n == nullptr) return fail(ERC_E_INVALID_ARG, "n is NULL");
+    *n = h->n;
+    return ERC_OK;
+  });
 }
 
 erc_status erc_num_edges(erc_handle h, int64_t* m) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (m == nullptr) return fail(ERC_E_INVALID_ARG, "m is NULL");
-  *m = h->m;
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (m == nullptr) return fail(ERC_E_INVALID_ARG, "m is NULL");
+    *m = h->m;
+    return ERC_OK;
+  });
 }
 
 erc_status erc_edge_endpoints(erc_handle h, int32_t* u_dev, int32_t* v_dev, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (h->m > 0 && (u_dev == nullptr || v_dev == nullptr)) return fail(ERC_E_INVALID_ARG, "output is NULL");
-  ERC_HIP(launch_endpoints(h->dg, u_dev, v_dev, static_cast<hipStream_t>(stream)));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (h->m > 0 && (u_dev == nullptr || v_dev == nullptr)) return fail(ERC_E_INVALID_ARG, "output is NULL");
+    ERC_HIP(launch_endpoints(h->dg, u_dev, v_dev, static_cast<hipStream_t>(stream)));
+    return ERC_OK;
+  });
 }
 
 erc_status erc_destroy(erc_handle h) {
-  g_last_error.clear();
-  if (h == nullptr) return ERC_OK;
-  if (h->pinned) (void)hipHostFree(h->pinned);
-  for (auto& ev : h->ev)
-    if (ev) (void)hipEventDestroy(ev);
-  for (auto& ev : h->prof)
-    if (ev) (void)hipEventDestroy(ev);
-  delete h;
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (h == nullptr) return ERC_OK;
+    if (h->pinned) (void)hipHostFree(h->pinned);
+    for (auto& ev : h->ev)
+      if (ev) (void)hipEventDestroy(ev);
+    for (auto& ev : h->prof)
+      if (ev) (void)hipEventDestroy(ev);
+    delete h;
+    return ERC_OK;
+  });
 }
 
 erc_status erc_workspace_bytes(erc_handle h, int32_t k_block, size_t* bytes) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
-  if (k_block < 1 || k_block > max_width(h->dt))
-    return fail(ERC_E_INVALID_ARG, "k_block out of range for the working precision");
-  *bytes = static_cast<size_t>(work_layout(h, padded_width(h->dt, k_block)).total);
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    if (k_block < 1 || k_block > max_width(h->dt))
+      return fail(ERC_E_INVALID_ARG, "k_block out of range for the working precision");
+    *bytes = static_cast<size_t>(work_layout(h, padded_width(h->dt, k_block)).total);
+    return ERC_OK;
+  });
 }
 
 erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws_dev, size_t ws_bytes,
                           double* R_dev, erc_solve_info* info, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  erc_status st = check_params(h, params);
-  if (st != ERC_OK) return st;
-  if (h->m > 0 && R_dev == nullptr) return fail(ERC_E_INVALID_ARG, "R_dev is NULL");
-  if (ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "ws_dev is NULL");
-  const int kb = padded_width(h->dt, params->k_block);
-  const WorkLayout L = work_layout(h, kb);
-  if (static_cast<int64_t>(ws_bytes) < L.total)
-    return fail(ERC_E_WORKSPACE, "workspace smaller than erc_workspace_bytes");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
-  st = prepare_work(h, w, L, s);
-  if (st != ERC_OK) return st;
-  hipEvent_t t0 = nullptr, t1 = nullptr;
-  ERC_HIP(hipEventCreate(&t0));
-  ERC_HIP(hipEventCreate(&t1));
-  ERC_HIP(hipEventRecord(t0, s));
-  BlockStats bs;
-  int blocks = 0;
-  for (int c0 = params->col_begin; c0 < params->col_end; c0 += params->k_block) {
-    const int nc = std::min(params->k_block, params->col_end - c0);
-    const int acc = (c0 == params->col_begin && !(params->flags & ERC_ACCUMULATE)) ? 0 : 1;
-    st = solve_block(h, params, w, c0, nc, h->m > 0 ? R_dev : nullptr, acc, nullptr, &bs, s);
-    if (st != ERC_OK) {
-      (void)hipEventDestroy(t0);
-      (void)hipEventDestroy(t1);
-      return st;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    erc_status st = check_params(h, params);
+    if (st != ERC_OK) return st;
+    if (h->m > 0 && R_dev == nullptr) return fail(ERC_E_INVALID_ARG, "R_dev is NULL");
+    if (ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "ws_dev is NULL");
+    const int kb = padded_width(h->dt, params->k_block);
+    const WorkLayout L = work_layout(h, kb);
+    if (static_cast<int64_t>(ws_bytes) < L.total)
+      return fail(ERC_E_WORKSPACE, "workspace smaller than erc_workspace_bytes");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    st = prepare_work(h, w, L, s);
+    if (st != ERC_OK) return st;
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    ERC_HIP(hipEventCreate(&t0));
+    ERC_HIP(hipEventCreate(&t1));
+    ERC_HIP(hipEventRecord(t0, s));
+    BlockStats bs;
+    int blocks = 0;
+    for (int c0 = params->col_begin; c0 < params->col_end; c0 += params->k_block) {
+      const int nc = std::min(params->k_block, params->col_end - c0);
+      const int acc = (c0 == params->col_begin && !(params->flags & ERC_ACCUMULATE)) ? 0 : 1;
+      st = solve_block(h, params, w, c0, nc, h->m > 0 ? R_dev : nullptr, acc, nullptr, &bs, s);
+      if (st != ERC_OK) {
+        (void)hipEventDestroy(t0);
+        (void)hipEventDestroy(t1);
+        return st;
+      }
+      ++blocks;
     }
-    ++blocks;
-  }
-  int64_t bad = 0;
-  if (h->m > 0) {
-    ERC_HIP(launch_count_bad(R_dev, h->m, w, s));
-    double hb = 0.0;
-    ERC_HIP(hipMemcpyAsync(reinterpret_cast<double*>(h->pinned + 2), w.out, 8, hipMemcpyDeviceToHost, s));
-    ERC_HIP(hipEventRecord(t1, s));
-    ERC_HIP(hipStreamSynchronize(s));
-    std::memcpy(&hb, h->pinned + 2, 8);
-    bad = static_cast<int64_t>(hb);
-  } else {
-    ERC_HIP(hipEventRecord(t1, s));
-    ERC_HIP(hipStreamSynchronize(s));
-  }
-  float total = 0.0f;
-  (void)hipEventElapsedTime(&total, t0, t1);  // timing only: 0 if unavailable
-  (void)hipEventDestroy(t0);
-  (void)hipEventDestroy(t1);
-  if (info) {
-    info->blocks = blocks;
-    info->iters_max = bs.iters_max;
-    info->cols_unconverged = bs.unconverged;
-    info->breakdowns = bs.breakdowns;
-    info->iters_total = bs.iters_total;
-    info->launches = bs.launches;
-    info->nonpositive = bad;
-    info->max_final_relres = bs.max_relres;
-    info->ms_rhs = bs.ms_rhs;
-    info->ms_cg = bs.ms_cg;
-    info->ms_accum = bs.ms_accum;
-    info->ms_total = total;
-    info->ms_spmm = bs.ms_spmm;
-    info->spmm_timed = bs.spmm_timed;
-    info->spmm_full = bs.spmm_full;
-    // algorithmic bytes (no neighbour-row gathers beyond one read of each vector): every
-    // SpMM that found active columns reads col (+ w), rowptr, p and r and writes q; its
-    // update reads z, r, p, q and writes z, r, p; per block the right-hand sides read
-    // col, eid (+ w) and write z, r, p, and the edge distances read the upper col
-    // entries and z and read-modify-write R
-    {
-      const double sz = static_cast<double>(dsize(h->dt));
-      const double n = static_cast<double>(h->n), nnz = static_cast<double>(h->nnz);
-      const double m = static_cast<double>(h->m);
-      const double kb = static_cast<double>(padded_width(h->dt, params->k_block));
-      const double wb = h->weighted ? sz : 0.0;
-      const double spmm = (4.0 + wb) * nnz + 8.0 * (n + 1) + 3.0 * sz * n * kb;
-      const double upd = 7.0 * sz * n * kb;
-      const double rhs = (8.0 + wb) * nnz + 3.0 * sz * n * kb;
-      const double ed = 2.0 * nnz + sz * n * kb + 16.0 * m;
-      info->bytes_model = static_cast<double>(bs.spmm_full) * (spmm + upd) +
-                          static_cast<double>(blocks) * (rhs + ed);
+    int64_t bad = 0;
+    if (h->m > 0) {
+      ERC_HIP(launch_count_bad(R_dev, h->m, w, s));
+      double hb = 0.0;
+      ERC_HIP(hipMemcpyAsync(reinterpret_cast<double*>(h->pinned + 2), w.out, 8, hipMemcpyDeviceToHost, s));
+      ERC_HIP(hipEventRecord(t1, s));
+      ERC_HIP(hipStreamSynchronize(s));
+      std::memcpy(&hb, h->pinned + 2, 8);
+      bad = static_cast<int64_t>(hb);
+    } else {
+      ERC_HIP(hipEventRecord(t1, s));
+      ERC_HIP(hipStreamSynchronize(s));
     }
-  }
-  if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown in " + std::to_string(bs.breakdowns) + " column(s)");
-  if (bad > 0) return fail(ERC_E_NUMERIC, std::to_string(bad) + " resistance(s) <= 0 or not finite");
-  if (bs.unconverged > 0)
-    return fail(ERC_E_NOT_CONVERGED, std::to_string(bs.unconverged) + " column(s) reached max_iter");
-  return ERC_OK;
+    float total = 0.0f;
+    (void)hipEventElapsedTime(&total, t0, t1);  // timing only: 0 if unavailable
+    (void)hipEventDestroy(t0);
+    (void)hipEventDestroy(t1);
+    if (info) {
+      info->blocks = blocks;
+      info->iters_max = bs.iters_max;
+      info->cols_unconverged = bs.unconverged;
+      info->breakdowns = bs.breakdowns;
+      info->iters_total = bs.iters_total;
+      info->launches = bs.launches;
+      info->nonpositive = bad;
+      info->max_final_relres = bs.max_relres;
+      info->ms_rhs = bs.ms_rhs;
+      info->ms_cg = bs.ms_cg;
+      info->ms_accum = bs.ms_accum;
+      info->ms_total = total;
+      info->ms_spmm = bs.ms_spmm;
+      info->spmm_timed = bs.spmm_timed;
+      info->spmm_full = bs.spmm_full;
+      // algorithmic bytes (no neighbour-row gathers beyond one read of each vector): every
+      // SpMM that found active columns reads col (+ w), rowptr, p and r and writes q; its
+      // update reads z, r, p, q and writes z, r, p; per block the right-hand sides read
+      // col, eid (+ w) and write z, r, p, and the edge distances read the upper col
+      // entries and z and read-modify-write R
+      {
+        const double sz = static_cast<double>(dsize(h->dt));
+        const double n = static_cast<double>(h->n), nnz = static_cast<double>(h->nnz);
+        const double m = static_cast<double>(h->m);
+        const double kb = static_cast<double>(padded_width(h->dt, params->k_block));
+        const double wb = h->weighted ? sz : 0.0;
+        const double spmm = (4.0 + wb) * nnz + 8.0 * (n + 1) + 3.0 * sz * n * kb;
+        const double upd = 7.0 * sz * n * kb;
+        const double rhs = (8.0 + wb) * nnz + 3.0 * sz * n * kb;
+        const double ed = 2.0 * nnz + sz * n * kb + 16.0 * m;
+        info->bytes_model = static_cast<double>(bs.spmm_full) * (spmm + upd) +
+                            static_cast<double>(blocks) * (rhs + ed);
+      }
+    }
+    if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown in " + std::to_string(bs.breakdowns) + " column(s)");
+    if (bad > 0) return fail(ERC_E_NUMERIC, std::to_string(bad) + " resistance(s) <= 0 or not finite");
+    if (bs.unconverged > 0)
+      return fail(ERC_E_NOT_CONVERGED, std::to_string(bs.unconverged) + " column(s) reached max_iter");
+    return ERC_OK;
+  });
 }
 
 erc_status erc_curvature(erc_handle h, const double* R_dev, double* p_dev, double* kappa_dev,
                          void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (p_dev == nullptr || (h->m > 0 && (R_dev == nullptr || kappa_dev == nullptr)))
-    return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  ERC_HIP(launch_node_p(h->dg, h->dt, R_dev, p_dev, s));
-  ERC_HIP(launch_edge_kappa(h->dg, R_dev, p_dev, kappa_dev, s));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (p_dev == nullptr || (h->m > 0 && (R_dev == nullptr || kappa_dev == nullptr)))
+      return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ERC_HIP(launch_node_p(h->dg, h->dt, R_dev, p_dev, s));
+    ERC_HIP(launch_edge_kappa(h->dg, R_dev, p_dev, kappa_dev, s));
+    return ERC_OK;
+  });
 }
 
 namespace {
@@ -977,38 +1119,42 @@ SampleLayout sample_layout(const erc_graph_s* h) {
 }  // namespace
 
 erc_status erc_sampling_scratch_bytes(erc_handle h, size_t* bytes) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
-  *bytes = static_cast<size_t>(sample_layout(h).total);
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    *bytes = static_cast<size_t>(sample_layout(h).total);
+    return ERC_OK;
+  });
 }
 
 erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta, void* scratch_dev,
                               size_t scratch_bytes, double* node_prob_dev, double* edge_prob_dev,
                               void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (!(eta > 0.0) || !std::isfinite(eta)) return fail(ERC_E_INVALID_ARG, "eta must be finite and > 0");
-  if (node_prob_dev == nullptr || scratch_dev == nullptr ||
-      (h->m > 0 && (kappa_dev == nullptr || edge_prob_dev == nullptr)))
-    return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  const SampleLayout L = sample_layout(h);
-  if (static_cast<int64_t>(scratch_bytes) < L.total)
-    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_sampling_scratch_bytes");
-  char* b = static_cast<char*>(scratch_dev);
-  SampleWork sw{};
-  sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
-  sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
-  sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
-  sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
-  sw.totals = reinterpret_cast<double*>(b + L.totals);
-  sw.grid = L.grid;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
-  ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
-  ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (!(eta > 0.0) || !std::isfinite(eta)) return fail(ERC_E_INVALID_ARG, "eta must be finite and > 0");
+    if (node_prob_dev == nullptr || scratch_dev == nullptr ||
+        (h->m > 0 && (kappa_dev == nullptr || edge_prob_dev == nullptr)))
+      return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    const SampleLayout L = sample_layout(h);
+    if (static_cast<int64_t>(scratch_bytes) < L.total)
+      return fail(ERC_E_WORKSPACE, "scratch smaller than erc_sampling_scratch_bytes");
+    char* b = static_cast<char*>(scratch_dev);
+    SampleWork sw{};
+    sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
+    sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
+    sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
+    sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
+    sw.totals = reinterpret_cast<double*>(b + L.totals);
+    sw.grid = L.grid;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
+    ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
+    ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
+    return ERC_OK;
+  });
 }
 
 namespace {
@@ -1057,244 +1203,262 @@ erc_status read_status(uint32_t* status_dev, hipStream_t s, uint32_t* out) {
 }  // namespace
 
 erc_status erc_draw_scratch_bytes(erc_handle h, erc_items items, size_t* bytes) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
-  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
-  *bytes = static_cast<size_t>(draw_layout(items == ERC_NODES ? h->n : h->m).total);
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+    *bytes = static_cast<size_t>(draw_layout(items == ERC_NODES ? h->n : h->m).total);
+    return ERC_OK;
+  });
 }
 
 erc_status erc_draw(erc_handle h, erc_items items, const double* prob_dev, int64_t draws,
                     uint64_t seed, void* scratch_dev, size_t scratch_bytes, int64_t* idx_dev,
                     void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
-  const int64_t N = items == ERC_NODES ? h->n : h->m;
-  if (N <= 0) return fail(ERC_E_INVALID_ARG, "no items to draw from");
-  if (draws < 0) return fail(ERC_E_INVALID_ARG, "draws must be >= 0");
-  if (prob_dev == nullptr || scratch_dev == nullptr || (draws > 0 && idx_dev == nullptr))
-    return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  const DrawLayout L = draw_layout(N);
-  if (static_cast<int64_t>(scratch_bytes) < L.total)
-    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_draw_scratch_bytes");
-  char* b = static_cast<char*>(scratch_dev);
-  DrawWork w{};
-  w.cdf = reinterpret_cast<uint64_t*>(b + L.cdf);
-  w.bsum = reinterpret_cast<uint64_t*>(b + L.bsum);
-  w.psum = reinterpret_cast<double*>(b + L.psum);
-  w.status = reinterpret_cast<uint32_t*>(b + L.status);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
-  ERC_HIP(launch_draw(prob_dev, N, draws, splitmix_first(seed), w, idx_dev, s));
-  uint32_t st = 0;
-  erc_status rs = read_status(w.status, s, &st);
-  if (rs != ERC_OK) return rs;
-  if (st & kDrawBadProb) return fail(ERC_E_NUMERIC, "a probability is NaN or outside [0, 1]");
-  if (st & kDrawSumTooLarge) return fail(ERC_E_NUMERIC, "probabilities sum above 1.5");
-  if (st & kDrawAllZero) return fail(ERC_E_NUMERIC, "every probability rounds to a zero weight");
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+    const int64_t N = items == ERC_NODES ? h->n : h->m;
+    if (N <= 0) return fail(ERC_E_INVALID_ARG, "no items to draw from");
+    if (draws < 0) return fail(ERC_E_INVALID_ARG, "draws must be >= 0");
+    if (prob_dev == nullptr || scratch_dev == nullptr || (draws > 0 && idx_dev == nullptr))
+      return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    const DrawLayout L = draw_layout(N);
+    if (static_cast<int64_t>(scratch_bytes) < L.total)
+      return fail(ERC_E_WORKSPACE, "scratch smaller than erc_draw_scratch_bytes");
+    char* b = static_cast<char*>(scratch_dev);
+    DrawWork w{};
+    w.cdf = reinterpret_cast<uint64_t*>(b + L.cdf);
+    w.bsum = reinterpret_cast<uint64_t*>(b + L.bsum);
+    w.psum = reinterpret_cast<double*>(b + L.psum);
+    w.status = reinterpret_cast<uint32_t*>(b + L.status);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
+    ERC_HIP(launch_draw(prob_dev, N, draws, splitmix_first(seed), w, idx_dev, s));
+    uint32_t st = 0;
+    erc_status rs = read_status(w.status, s, &st);
+    if (rs != ERC_OK) return rs;
+    if (st & kDrawBadProb) return fail(ERC_E_NUMERIC, "a probability is NaN or outside [0, 1]");
+    if (st & kDrawSumTooLarge) return fail(ERC_E_NUMERIC, "probabilities sum above 1.5");
+    if (st & kDrawAllZero) return fail(ERC_E_NUMERIC, "every probability rounds to a zero weight");
+    return ERC_OK;
+  });
 }
 
 erc_status erc_subgraph_scratch_bytes(erc_handle h, size_t* bytes) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
-  *bytes = static_cast<size_t>(sub_layout(h).total);
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    *bytes = static_cast<size_t>(sub_layout(h).total);
+    return ERC_OK;
+  });
 }
 
 erc_status erc_subgraph(erc_handle h, erc_items items, const int64_t* idx_dev, int64_t count,
                         void* scratch_dev, size_t scratch_bytes, int32_t* nodes_dev,
                         int64_t* edges_dev, int32_t* u_dev, int32_t* v_dev,
                         int64_t* counts_host, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
-  if (count < 0) return fail(ERC_E_INVALID_ARG, "count must be >= 0");
-  if (scratch_dev == nullptr || counts_host == nullptr || nodes_dev == nullptr ||
-      (count > 0 && idx_dev == nullptr) ||
-      (h->m > 0 && (edges_dev == nullptr || u_dev == nullptr || v_dev == nullptr)))
-    return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  if (items == ERC_EDGES && h->m == 0 && count > 0)
-    return fail(ERC_E_INVALID_ARG, "the graph has no edges");
-  const SubLayout L = sub_layout(h);
-  if (static_cast<int64_t>(scratch_bytes) < L.total)
-    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_subgraph_scratch_bytes");
-  char* b = static_cast<char*>(scratch_dev);
-  SubgraphWork w{};
-  w.npos = reinterpret_cast<uint32_t*>(b + L.npos);
-  w.epos = reinterpret_cast<uint32_t*>(b + L.epos);
-  w.bsum = reinterpret_cast<uint32_t*>(b + L.bsum);
-  w.status = reinterpret_cast<uint32_t*>(b + L.status);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
-  ERC_HIP(launch_subgraph(h->dg, items == ERC_NODES ? 0 : 1, idx_dev, count, w, nodes_dev,
-                          edges_dev, u_dev, v_dev, s));
-  uint32_t tot[2] = {0u, 0u};
-  ERC_HIP(hipMemcpyAsync(&tot[0], w.npos + h->n, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
-  ERC_HIP(hipMemcpyAsync(&tot[1], w.epos + h->m, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
-  uint32_t st = 0;
-  erc_status rs = read_status(w.status, s, &st);
-  if (rs != ERC_OK) return rs;
-  if (st & kSubBadIndex) return fail(ERC_E_INVALID_ARG, "a drawn index is out of range");
-  counts_host[0] = tot[0];
-  counts_host[1] = tot[1];
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (items != ERC_NODES && items != ERC_EDGES) return fail(ERC_E_INVALID_ARG, "items must be ERC_NODES or ERC_EDGES");
+    if (count < 0) return fail(ERC_E_INVALID_ARG, "count must be >= 0");
+    if (scratch_dev == nullptr || counts_host == nullptr || nodes_dev == nullptr ||
+        (count > 0 && idx_dev == nullptr) ||
+        (h->m > 0 && (edges_dev == nullptr || u_dev == nullptr || v_dev == nullptr)))
+      return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    if (items == ERC_EDGES && h->m == 0 && count > 0)
+      return fail(ERC_E_INVALID_ARG, "the graph has no edges");
+    const SubLayout L = sub_layout(h);
+    if (static_cast<int64_t>(scratch_bytes) < L.total)
+      return fail(ERC_E_WORKSPACE, "scratch smaller than erc_subgraph_scratch_bytes");
+    char* b = static_cast<char*>(scratch_dev);
+    SubgraphWork w{};
+    w.npos = reinterpret_cast<uint32_t*>(b + L.npos);
+    w.epos = reinterpret_cast<uint32_t*>(b + L.epos);
+    w.bsum = reinterpret_cast<uint32_t*>(b + L.bsum);
+    w.status = reinterpret_cast<uint32_t*>(b + L.status);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    ERC_HIP(launch_fill_u32(w.status, 0u, 1, s));
+    ERC_HIP(launch_subgraph(h->dg, items == ERC_NODES ? 0 : 1, idx_dev, count, w, nodes_dev,
+                            edges_dev, u_dev, v_dev, s));
+    uint32_t tot[2] = {0u, 0u};
+    ERC_HIP(hipMemcpyAsync(&tot[0], w.npos + h->n, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    ERC_HIP(hipMemcpyAsync(&tot[1], w.epos + h->m, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    uint32_t st = 0;
+    erc_status rs = read_status(w.status, s, &st);
+    if (rs != ERC_OK) return rs;
+    if (st & kSubBadIndex) return fail(ERC_E_INVALID_ARG, "a drawn index is out of range");
+    counts_host[0] = tot[0];
+    counts_host[1] = tot[1];
+    return ERC_OK;
+  });
 }
 
 erc_status erc_debug_check_plan(const erc_graph_desc* desc) {
-  g_last_error.clear();
-  Canon c;
-  erc_status st = canonicalise(desc, &c);
-  if (st != ERC_OK) return st;
-  const int64_t n = desc->n;
-  const int64_t* rp = desc->rowptr;
-  const int64_t nnz = rp[n];
-  const Shape s = make_shape(n, nnz);
-  Plan P;
-  build_plan(desc, c, s, &P);
-  auto bad = [&](const std::string& what) { return fail(ERC_E_STATE, "plan check: " + what); };
-  const int64_t nt = static_cast<int64_t>(P.task_row.size());
-  const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
-  const int64_t np = static_cast<int64_t>(P.piece_row.size());
-  if (nt > s.ntask_max || nm > s.nmega_max || np > s.npiece_max || P.nslot > s.nslot_max)
-    return bad("list exceeds its size bound");
-  if (s.grid < 1 || s.grid > kMaxSpmmGrid || s.waves != s.grid * kWavesPerBlock)
-    return bad("grid shape");
-  // SpMM coverage: each entry once, by a light row or by a block task
-  std::vector<unsigned char> cover(nnz, 0);
-  const int64_t nl = static_cast<int64_t>(P.light.size());
-  if (static_cast<int64_t>(P.wave_lo.size()) != s.waves + 1 || P.wave_lo[0] != 0 ||
-      P.wave_lo[s.waves] != nl)
-    return bad("wave ranges do not span the light rows");
-  for (int w = 0; w < s.waves; ++w)
-    if (P.wave_lo[w] > P.wave_lo[w + 1]) return bad("wave ranges not monotone");
-  std::vector<unsigned char> is_light(n, 0);
-  for (int64_t k = 0; k < nl; ++k) {
-    const int64_t i = P.light[k];
-    if (i < 0 || i >= n || (k > 0 && P.light[k - 1] >= i)) return bad("light rows not ascending in range");
-    if (rp[i + 1] - rp[i] > s.heavy) return bad("light row above the heavy threshold");
-    is_light[i] = 1;
-    for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) cover[pos] += 1;
-  }
-  std::vector<int32_t> seen_chunks(nm, 0);
-  for (int64_t t = 0; t < nt; ++t) {
-    const int64_t i = P.task_row[t];
-    if (i < 0 || i >= n || is_light[i]) return bad("task row out of range or also light");
-    if (P.task_beg[t] < rp[i] || P.task_end[t] > rp[i + 1] || P.task_beg[t] >= P.task_end[t])
-      return bad("task range outside its row");
-    const int32_t mh = P.task_mega[t];
-    if (mh >= 0) {
-      if (mh >= nm || P.task_chunk[t] < 0 || P.task_chunk[t] >= P.mega_nchunk[mh])
-        return bad("chunk index out of range");
-      if (P.mega_chunk0[mh] + P.mega_nchunk[mh] > P.nslot) return bad("chunk slots out of range");
-      seen_chunks[mh] += 1;
-    } else if (P.task_beg[t] != rp[i] || P.task_end[t] != rp[i + 1]) {
-      return bad("single-chunk task does not cover its row");
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    Canon c;
+    erc_status st = canonicalise(desc, &c);
+    if (st != ERC_OK) return st;
+    const int64_t n = desc->n;
+    const int64_t* rp = desc->rowptr;
+    const int64_t nnz = rp[n];
+    const Shape s = make_shape(n, nnz);
+    Plan P;
+    build_plan(desc, c, s, &P);
+    auto bad = [&](const std::string& what) { return fail(ERC_E_STATE, "plan check: " + what); };
+    const int64_t nt = static_cast<int64_t>(P.task_row.size());
+    const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
+    const int64_t np = static_cast<int64_t>(P.piece_row.size());
+    if (nt > s.ntask_max || nm > s.nmega_max || np > s.npiece_max || P.nslot > s.nslot_max)
+      return bad("list exceeds its size bound");
+    if (s.grid < 1 || s.grid > kMaxSpmmGrid || s.waves != s.grid * kWavesPerBlock)
+      return bad("grid shape");
+    // SpMM coverage: each entry once, by a light row or by a block task
+    std::vector<unsigned char> cover(nnz, 0);
+    const int64_t nl = static_cast<int64_t>(P.light.size());
+    if (static_cast<int64_t>(P.wave_lo.size()) != s.waves + 1 || P.wave_lo[0] != 0 ||
+        P.wave_lo[s.waves] != nl)
+      return bad("wave ranges do not span the light rows");
+    for (int w = 0; w < s.waves; ++w)
+      if (P.wave_lo[w] > P.wave_lo[w + 1]) return bad("wave ranges not monotone");
+    std::vector<unsigned char> is_light(n, 0);
+    for (int64_t k = 0; k < nl; ++k) {
+      const int64_t i = P.light[k];
+      if (i < 0 || i >= n || (k > 0 && P.light[k - 1] >= i)) return bad("light rows not ascending in range");
+      if (rp[i + 1] - rp[i] > s.heavy) return bad("light row above the heavy threshold");
+      is_light[i] = 1;
+      for (int64_t pos = rp[i]; pos < rp[i + 1]; ++pos) cover[pos] += 1;
     }
-    for (int64_t pos = P.task_beg[t]; pos < P.task_end[t]; ++pos) cover[pos] += 1;
-  }
-  for (int64_t mh = 0; mh < nm; ++mh)
-    if (seen_chunks[mh] != P.mega_nchunk[mh]) return bad("multi-chunk row missing chunks");
-  for (int64_t i = 0; i < n; ++i)
-    if (!is_light[i] && rp[i + 1] - rp[i] <= s.heavy) return bad("row in no plan list");
-  for (int64_t pos = 0; pos < nnz; ++pos)
-    if (cover[pos] != 1) return bad("entry not covered exactly once");
-  // edge pieces: each upper entry once, edge ids consistent with eid
-  std::fill(cover.begin(), cover.end(), 0);
-  for (int64_t t = 0; t < np; ++t) {
-    const int64_t u = P.piece_row[t];
-    if (u < 0 || u >= n) return bad("piece row out of range");
-    const int64_t up = c.ubase[u + 1] - c.ubase[u];
-    const int64_t upos = rp[u + 1] - up;
-    if (P.piece_beg[t] < upos || P.piece_end[t] > rp[u + 1] || P.piece_beg[t] >= P.piece_end[t])
-      return bad("piece outside the upper entries of its row");
-    for (int64_t pos = P.piece_beg[t]; pos < P.piece_end[t]; ++pos) {
-      if (desc->col[pos] <= u) return bad("piece covers a lower entry");
-      const int64_t e = c.ubase[u] + (pos - upos);
-      if (e != c.eid[pos]) return bad("piece edge id differs from the entry's edge id");
-      cover[pos] += 1;
+    std::vector<int32_t> seen_chunks(nm, 0);
+    for (int64_t t = 0; t < nt; ++t) {
+      const int64_t i = P.task_row[t];
+      if (i < 0 || i >= n || is_light[i]) return bad("task row out of range or also light");
+      if (P.task_beg[t] < rp[i] || P.task_end[t] > rp[i + 1] || P.task_beg[t] >= P.task_end[t])
+        return bad("task range outside its row");
+      const int32_t mh = P.task_mega[t];
+      if (mh >= 0) {
+        if (mh >= nm || P.task_chunk[t] < 0 || P.task_chunk[t] >= P.mega_nchunk[mh])
+          return bad("chunk index out of range");
+        if (P.mega_chunk0[mh] + P.mega_nchunk[mh] > P.nslot) return bad("chunk slots out of range");
+        seen_chunks[mh] += 1;
+      } else if (P.task_beg[t] != rp[i] || P.task_end[t] != rp[i + 1]) {
+        return bad("single-chunk task does not cover its row");
+      }
+      for (int64_t pos = P.task_beg[t]; pos < P.task_end[t]; ++pos) cover[pos] += 1;
     }
-  }
-  for (int64_t u = 0; u < n; ++u)
-    for (int64_t pos = rp[u]; pos < rp[u + 1]; ++pos)
-      if ((desc->col[pos] > u) != (cover[pos] == 1)) return bad("upper entry not covered exactly once");
-  return ERC_OK;
+    for (int64_t mh = 0; mh < nm; ++mh)
+      if (seen_chunks[mh] != P.mega_nchunk[mh]) return bad("multi-chunk row missing chunks");
+    for (int64_t i = 0; i < n; ++i)
+      if (!is_light[i] && rp[i + 1] - rp[i] <= s.heavy) return bad("row in no plan list");
+    for (int64_t pos = 0; pos < nnz; ++pos)
+      if (cover[pos] != 1) return bad("entry not covered exactly once");
+    // edge pieces: each upper entry once, edge ids consistent with eid
+    std::fill(cover.begin(), cover.end(), 0);
+    for (int64_t t = 0; t < np; ++t) {
+      const int64_t u = P.piece_row[t];
+      if (u < 0 || u >= n) return bad("piece row out of range");
+      const int64_t up = c.ubase[u + 1] - c.ubase[u];
+      const int64_t upos = rp[u + 1] - up;
+      if (P.piece_beg[t] < upos || P.piece_end[t] > rp[u + 1] || P.piece_beg[t] >= P.piece_end[t])
+        return bad("piece outside the upper entries of its row");
+      for (int64_t pos = P.piece_beg[t]; pos < P.piece_end[t]; ++pos) {
+        if (desc->col[pos] <= u) return bad("piece covers a lower entry");
+        const int64_t e = c.ubase[u] + (pos - upos);
+        if (e != c.eid[pos]) return bad("piece edge id differs from the entry's edge id");
+        cover[pos] += 1;
+      }
+    }
+    for (int64_t u = 0; u < n; ++u)
+      for (int64_t pos = rp[u]; pos < rp[u + 1]; ++pos)
+        if ((desc->col[pos] > u) != (cover[pos] == 1)) return bad("upper entry not covered exactly once");
+    return ERC_OK;
+  });
 }
 
 erc_status erc_debug_edge_ids(erc_handle h, int32_t* eid_dev, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (h->nnz > 0 && eid_dev == nullptr) return fail(ERC_E_INVALID_ARG, "eid_dev is NULL");
-  ERC_HIP(launch_eids(h->dg, eid_dev, static_cast<hipStream_t>(stream)));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (h->nnz > 0 && eid_dev == nullptr) return fail(ERC_E_INVALID_ARG, "eid_dev is NULL");
+    ERC_HIP(launch_eids(h->dg, eid_dev, static_cast<hipStream_t>(stream)));
+    return ERC_OK;
+  });
 }
 
 erc_status erc_debug_rhs(erc_handle h, int32_t K_total, int32_t col0, int32_t ncols, uint64_t seed,
                          void* Y_dev, void* ws_dev, size_t ws_bytes, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (K_total < 1 || ncols < 1 || ncols > max_width(h->dt) || col0 < 0 || col0 + ncols > K_total)
-    return fail(ERC_E_INVALID_ARG, "bad column range");
-  if (Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  const int kb = padded_width(h->dt, ncols);
-  const WorkLayout L = work_layout(h, kb);
-  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, kb, ws_dev, L);
-  erc_status st = prepare_work(h, w, L, s);
-  if (st != ERC_OK) return st;
-  ERC_HIP(launch_rhs(h->dg, w, h->dt, K_total, col0, ncols, splitmix_first(seed),
-                     1.0 / std::sqrt(static_cast<double>(K_total)), 0.5, s));
-  ERC_HIP(launch_copy_cols(h->dg, w.r, kb, h->dt, ncols, Y_dev, s));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (K_total < 1 || ncols < 1 || ncols > max_width(h->dt) || col0 < 0 || col0 + ncols > K_total)
+      return fail(ERC_E_INVALID_ARG, "bad column range");
+    if (Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    const int kb = padded_width(h->dt, ncols);
+    const WorkLayout L = work_layout(h, kb);
+    if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Work w = carve_work(h, kb, ws_dev, L);
+    erc_status st = prepare_work(h, w, L, s);
+    if (st != ERC_OK) return st;
+    ERC_HIP(launch_rhs(h->dg, w, h->dt, K_total, col0, ncols, splitmix_first(seed),
+                       1.0 / std::sqrt(static_cast<double>(K_total)), 0.5, s));
+    ERC_HIP(launch_copy_cols(h->dg, w.r, kb, h->dt, ncols, Y_dev, s));
+    return ERC_OK;
+  });
 }
 
 erc_status erc_debug_spmm(erc_handle h, double delta, int32_t ncols, const void* X_dev, void* Y_dev,
                           void* ws_dev, size_t ws_bytes, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  if (ncols < 1 || ncols > max_width(h->dt) || padded_width(h->dt, ncols) != ncols)
-    return fail(ERC_E_INVALID_ARG, "ncols must be a padded block width");
-  if (!std::isfinite(delta) || delta < 0.0) return fail(ERC_E_INVALID_ARG, "delta must be finite and >= 0");
-  if (X_dev == nullptr || Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  const WorkLayout L = work_layout(h, ncols);
-  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, ncols, ws_dev, L);
-  erc_status st = prepare_work(h, w, L, s);
-  if (st != ERC_OK) return st;
-  ERC_HIP(launch_spmm(h->dg, w, h->dt, delta, X_dev, X_dev, Y_dev, w.cs.one, s));
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    if (ncols < 1 || ncols > max_width(h->dt) || padded_width(h->dt, ncols) != ncols)
+      return fail(ERC_E_INVALID_ARG, "ncols must be a padded block width");
+    if (!std::isfinite(delta) || delta < 0.0) return fail(ERC_E_INVALID_ARG, "delta must be finite and >= 0");
+    if (X_dev == nullptr || Y_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    const WorkLayout L = work_layout(h, ncols);
+    if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Work w = carve_work(h, ncols, ws_dev, L);
+    erc_status st = prepare_work(h, w, L, s);
+    if (st != ERC_OK) return st;
+    ERC_HIP(launch_spmm(h->dg, w, h->dt, delta, X_dev, X_dev, Y_dev, w.cs.one, s));
+    return ERC_OK;
+  });
 }
 
 erc_status erc_debug_solve_block(erc_handle h, const erc_solve_params* params, int32_t col0,
                                  int32_t ncols, void* ws_dev, size_t ws_bytes, void* Z_dev,
                                  int32_t* iters_host, void* stream) {
-  g_last_error.clear();
-  if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-  erc_status st = check_params(h, params);
-  if (st != ERC_OK) return st;
-  if (ncols < 1 || ncols > params->k_block || col0 < 0 || col0 + ncols > params->K_total)
-    return fail(ERC_E_INVALID_ARG, "bad column range");
-  if (Z_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
-  const int kb = padded_width(h->dt, params->k_block);
-  const WorkLayout L = work_layout(h, kb);
-  if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
-  st = prepare_work(h, w, L, s);
-  if (st != ERC_OK) return st;
-  BlockStats bs;
-  st = solve_block(h, params, w, col0, ncols, nullptr, 0, iters_host, &bs, s);
-  if (st != ERC_OK) return st;
-  ERC_HIP(launch_copy_cols(h->dg, w.z, kb, h->dt, ncols, Z_dev, s));
-  ERC_HIP(hipStreamSynchronize(s));
-  if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown");
-  if (bs.unconverged > 0) return fail(ERC_E_NOT_CONVERGED, "column(s) reached max_iter");
-  return ERC_OK;
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    erc_status st = check_params(h, params);
+    if (st != ERC_OK) return st;
+    if (ncols < 1 || ncols > params->k_block || col0 < 0 || col0 + ncols > params->K_total)
+      return fail(ERC_E_INVALID_ARG, "bad column range");
+    if (Z_dev == nullptr || ws_dev == nullptr) return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    const int kb = padded_width(h->dt, params->k_block);
+    const WorkLayout L = work_layout(h, kb);
+    if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    st = prepare_work(h, w, L, s);
+    if (st != ERC_OK) return st;
+    BlockStats bs;
+    st = solve_block(h, params, w, col0, ncols, nullptr, 0, iters_host, &bs, s);
+    if (st != ERC_OK) return st;
+    ERC_HIP(launch_copy_cols(h->dg, w.z, kb, h->dt, ncols, Z_dev, s));
+    ERC_HIP(hipStreamSynchronize(s));
+    if (bs.breakdowns > 0) return fail(ERC_E_NUMERIC, "CG breakdown");
+    if (bs.unconverged > 0) return fail(ERC_E_NOT_CONVERGED, "column(s) reached max_iter");
+    return ERC_OK;
+  });
 }
 
 }  // extern "C"

@@ -129,6 +129,7 @@ def test_validate_fp64_weights_and_status_strings():
     assert _abi.erc_validate(d) == g.m
     assert _abi.erc_status_string(_abi.ERC_OK) == "ok"
     assert _abi.erc_status_string(_abi.ERC_E_NOT_CONVERGED) == "not converged"
+    assert _abi.erc_status_string(_abi.ERC_E_HOST) == "host allocation or thread failure"
 
 
 @pytest.mark.parametrize("name", ["er2k", "sbm20k", "cl170k"])
