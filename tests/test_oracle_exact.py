@@ -46,25 +46,31 @@ def test_laplacian_btwb_equals_d_minus_a(seed):
 
 
 def test_check_graph_rejects():
+    # each bad input breaks exactly one rule, and the message names that rule
     good = gen.cycle_graph(5)
     GR.check_graph(good)
     bad_sym = gen.CSRGraph(3, np.array([0, 1, 1, 1]), np.array([1], dtype=np.int32))
-    with pytest.raises(ValueError):
+    with pytest.raises(ValueError, match="symmetric"):
         GR.check_graph(bad_sym)
-    loop = gen.CSRGraph(2, np.array([0, 1, 2]), np.array([0, 0], dtype=np.int32))
-    with pytest.raises(ValueError):
+    # (0, 0), (0, 1), (1, 0): symmetric and ascending, with a self-loop
+    loop = gen.CSRGraph(2, np.array([0, 2, 3]), np.array([0, 1, 0], dtype=np.int32))
+    with pytest.raises(ValueError, match="self-loop"):
         GR.check_graph(loop)
+    # (0, 1) and (1, 0) stored twice each: symmetric, with repeats
+    repeat = gen.CSRGraph(2, np.array([0, 2, 4]), np.array([1, 1, 0, 0], dtype=np.int32))
+    with pytest.raises(ValueError, match="ascending"):
+        GR.check_graph(repeat)
     unsorted = gen.CSRGraph(3, np.array([0, 2, 3, 4]), np.array([2, 1, 0, 0], dtype=np.int32))
-    with pytest.raises(ValueError):
+    with pytest.raises(ValueError, match="ascending"):
         GR.check_graph(unsorted)
     g = gen.path_graph(3, w=np.array([1.0, 2.0]))
     w = g.w.copy()
     w[0] = -1.0
-    with pytest.raises(ValueError):
+    with pytest.raises(ValueError, match="positive"):
         GR.check_graph(gen.CSRGraph(g.n, g.rowptr, g.col, w))
     w = g.w.copy()
     w[0] = 5.0  # breaks w_ij == w_ji
-    with pytest.raises(ValueError):
+    with pytest.raises(ValueError, match="symmetric"):
         GR.check_graph(gen.CSRGraph(g.n, g.rowptr, g.col, w))
 
 

@@ -30,6 +30,7 @@ PINS_OF = {
     "accurate.py": [os.path.join(_T, "test_oracle_accurate.py")],
     "sampling.py": [os.path.join(_T, "test_oracle_sampling.py")],
     "agreement.py": [os.path.join(_T, "test_oracle_agreement.py")],
+    "parallel.py": [os.path.join(_T, "test_oracle_parallel.py")],
 }
 
 # (id, module, original text, planted text); the first occurrence is changed, which for
@@ -88,6 +89,14 @@ MUTANTS = [
      "eid = np.searchsorted(keys, hi * g.n + lo)"),
     ("pinv_resistance_sign", "exact.py", "return Lp[eu, eu] + Lp[ev, ev] - 2.0 * Lp[eu, ev]",
      "return Lp[eu, eu] + Lp[ev, ev] + 2.0 * Lp[eu, ev]"),
+    ("self_loop_accepted", "graph.py", "    if np.any(rows == col):\n        raise ValueError(\"self-loop\")",
+     "    if False:\n        raise ValueError(\"self-loop\")"),
+    ("repeated_entries_accepted", "graph.py", "if np.any(np.diff(key) <= 0):",
+     "if np.any(np.diff(key) < 0):"),
+    ("base_is_the_seed", "hashing.py", "return U64(splitmix64(seed, 1)[0])", "return U64(seed)"),
+    # the column-parallel driver
+    ("parallel_ranges_overlap", "parallel.py", "jobs = [(bounds[k], bounds[k + 1], prm,",
+     "jobs = [(bounds[k], min(bounds[k + 1] + 1, col_end), prm,"),
     # compensated dot products
     ("two_sum_error_term", "accurate.py", "e = (a - (s - z)) + (b - z)", "e = (a - (s - z)) - (b - z)"),
     # Table 2 metrics
