@@ -20,6 +20,8 @@ GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "sbm
 def test_mae_and_sign_by_hand():
     assert AG.mae([1.0, -2.0, 3.0], [1.5, -2.0, 2.0]) == pytest.approx(0.5)
     assert AG.sign_agreement([1.0, -1.0, 0.0, 2.0], [3.0, -2.0, 0.0, -1.0]) == 0.75
+    # zero is its own sign class: 0 against a negative (or a positive) disagrees
+    assert AG.sign_agreement([0.0, 2.0, -1.0], [-3.0, 1.0, 0.0]) == pytest.approx(1 / 3)
 
 
 def test_average_ranks_ties():

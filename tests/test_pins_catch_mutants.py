@@ -26,7 +26,8 @@ PINS_OF = {
                                              "test_oracle_pcg.py")],
     "hashing.py": [os.path.join(_T, "test_oracle_hash.py")],
     "graph.py": [os.path.join(_T, "test_oracle_exact.py")],
-    "exact.py": [os.path.join(_T, "test_oracle_exact.py")],
+    "exact.py": [os.path.join(_T, f) for f in ("test_oracle_exact.py", "test_oracle_pipeline.py",
+                                               "test_oracle_agreement.py")],
     "accurate.py": [os.path.join(_T, "test_oracle_accurate.py")],
     "sampling.py": [os.path.join(_T, "test_oracle_sampling.py")],
     "agreement.py": [os.path.join(_T, "test_oracle_agreement.py")],
@@ -97,7 +98,25 @@ MUTANTS = [
     # the column-parallel driver
     ("parallel_ranges_overlap", "parallel.py", "jobs = [(bounds[k], bounds[k + 1], prm,",
      "jobs = [(bounds[k], min(bounds[k + 1] + 1, col_end), prm,"),
+    ("dense_Q_scale", "exact.py", "np.arange(col0, col0 + ncols)) / math.sqrt(K)",
+     "np.arange(col0, col0 + ncols)) / K"),
+    ("reg_resistance_sign", "exact.py", "return M[eu, eu] + M[ev, ev] - 2.0 * M[eu, ev]",
+     "return M[eu, eu] + M[ev, ev] - M[eu, ev]"),
+    ("jl_dense_unshifted", "exact.py", "Z = np.linalg.solve(L + delta * np.eye(g.n), Y)",
+     "Z = np.linalg.lstsq(L, Y, rcond=None)[0]"),
+    # Table 2 metrics
+    ("pearson_uncentred", "agreement.py", "    da = a - a.mean()\n    db = b - b.mean()",
+     "    da = a\n    db = b"),
+    ("sign_zero_merged", "agreement.py",
+     "return float(np.mean(np.sign(np.asarray(a, np.float64)) == np.sign(np.asarray(b, np.float64))))",
+     "return float(np.mean((np.asarray(a, np.float64) > 0) == (np.asarray(b, np.float64) > 0)))"),
+    # subgraphs of the draws
+    ("node_subgraph_union", "sampling.py", "ekeep = keep[eu] & keep[ev]", "ekeep = keep[eu] | keep[ev]"),
+    ("relabel_from_one", "sampling.py", "new_id[nodes] = np.arange(nodes.size)",
+     "new_id[nodes] = np.arange(1, nodes.size + 1)"),
+    ("edge_subgraph_one_endpoint", "sampling.py", "    keep[ev[ekeep]] = True\n", ""),
     # compensated dot products
+    ("two_prod_low_part_dropped", "accurate.py", "    al = a - ah\n", "    al = 0.0 * a\n"),
     ("two_sum_error_term", "accurate.py", "e = (a - (s - z)) + (b - z)", "e = (a - (s - z)) - (b - z)"),
     # Table 2 metrics
     ("rank_ties_not_averaged", "agreement.py", "ranks[order[i:j + 1]] = 0.5 * (i + j) + 1.0",
