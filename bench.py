@@ -25,11 +25,13 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 
-# HBM traffic of one full SpMM launch on the 2.4M-node workload, from two rocprofv3
-# --pmc runs of this benchmark (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch, median
-# over full launches), each scaled by what the counter reads for a plain 1 GiB copy
-# kernel run in the same process (FETCH_SIZE x 2.0, WRITE_SIZE x 1.0).  Valid only for
-# the kernel source it was measured on: reported as null once that file changes.
+# L2-to-fabric traffic of one full SpMM launch on the 2.4M-node workload, from two
+# rocprofv3 --pmc runs of this benchmark (FETCH_SIZE, then WRITE_SIZE, KiB per
+# dispatch, median over full launches), each scaled by what the counter reads for a
+# plain copy kernel of known size run in the same process (FETCH_SIZE x 2.0,
+# WRITE_SIZE x 1.0).  The counters count every request that leaves the L2, served by
+# the Infinity Cache or by HBM alike.  Valid only for the sources it was measured on:
+# reported as null once they change (the hash is only ever updated with new counters).
 MEASURED_TRAFFIC = {
     "workload": "cl2400k",
     "source_sha256_16": "d0cf3eae15d6ac09",
@@ -43,12 +45,37 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def elem_bytes(dtype: str) -> int:
+    return 4 if dtype == "f32" else 8
+
+
 def spmm_bytes_per_launch(g, kb: int, dtype: str) -> int:
-    """Algorithmic bytes of one SpMM launch: column indices (+ weights), row pointers,
-    and one pass each over p (read), r (read, for r.q) and q (write) of width kb."""
-    s = 4 if dtype == "f32" else 8
+    """Compulsory bytes of one SpMM launch: column indices (4 B per stored entry) and,
+    on weighted graphs, weights in the working precision, row pointers, one n-vector of
+    the diagonal, one read of p and one write of q (n x kb each).  Neighbour-row gathers
+    beyond that one read of p are not counted."""
+    s = elem_bytes(dtype)
+    per_nnz = 4 + (s if g.w is not None else 0)
+    return per_nnz * g.nnz + 8 * (g.n + 1) + s * g.n + 2 * s * g.n * kb
+
+
+def spmm_fused_bytes_per_launch(g, kb: int, dtype: str) -> int:
+    """What this SpMM kernel reads and writes once: column indices (+ weights), row
+    pointers, p, r (read for the fused r.q) and q; it forms q_i = delta p_i +
+    sum_j w_ij (p_i - p_j) without a stored diagonal."""
+    s = elem_bytes(dtype)
     per_nnz = 4 + (s if g.w is not None else 0)
     return per_nnz * g.nnz + 8 * (g.n + 1) + 3 * s * g.n * kb
+
+
+def iteration_bytes(g, kb: int, dtype: str) -> int:
+    """Algorithmic bytes of one CG iteration of one block: 4 nnz (+ s nnz) + 8 (n+1) +
+    s n + 11 s n kb, i.e. the SpMM's compulsory bytes and the vector passes of a
+    textbook iteration (SpMM: p read, q written; z, r update: z, p, r, q read, z, r
+    written; p update: r, p read, p written).  The fused kernels here make 10 passes."""
+    s = elem_bytes(dtype)
+    per_nnz = 4 + (s if g.w is not None else 0)
+    return per_nnz * g.nnz + 8 * (g.n + 1) + s * g.n + 11 * s * g.n * kb
 
 
 def kernel_source_hash() -> str:
@@ -70,22 +97,73 @@ def padded(kb: int, dtype: str) -> int:
     return w
 
 
-def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 25, cg_iters: int = 16):
-    """Time the CPU oracle on a bounded sample of this workload and scale to edges/s.
+_CPU = {}
+
+
+def _cpu_init():
+    from threadpoolctl import threadpool_limits
+
+    threadpool_limits(limits=1)  # one thread per oracle process
+
+
+def _cpu_rhs(args):
+    from oracle import erc as OE
+
+    c0, nc = args
+    gs, p = _CPU["g"], _CPU["p"]
+    return c0, OE.rhs(gs, p.K, c0, nc, p.seed, p.dtype)
+
+
+def _cpu_cg(args):
+    from oracle import erc as OE
+
+    c0, c1 = args
+    res = OE.cg_columns(_CPU["L"], _CPU["p"].delta, _CPU["Y"][:, c0:c1], 1e-300, _CPU["iters"])
+    return c0, res.Z
+
+
+def host_cpu():
+    """CPU model, logical CPUs and the CPUs this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    return {"model": model, "nproc": os.cpu_count() or 1, "usable": usable}
+
+
+def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 25, cg_iters: int = 16,
+                 procs: int = 0):
+    """Time the CPU oracle, column-parallel on the host's cores, on a bounded sample of
+    this workload and scale to edges/s.
 
     Sample: a 1/`scale_div` instance of the same graph recipe (n and m divided by
-    `scale_div`, the generator's offset i0 scaled with n), on which the oracle runs every
-    stage: Laplacian assembly, one block of right-hand sides, `cg_iters` CG iterations
-    of one full block, one block of edge distances, curvature and sampling.  Each stage
-    is scaled linearly in the graph size (stored entries or edges), RHS and distances by
-    the number of blocks, and CG by the column-iterations the GPU run took.
+    `scale_div`, the generator's offset i0 scaled with n).  The oracle runs one block of
+    right-hand sides and `cg_iters` CG iterations of one full block split into column
+    ranges over `procs` processes (one thread each; the columns are independent, as in
+    Algorithm 1), and Laplacian assembly, one block of edge distances, curvature and
+    sampling in one process.  Each stage is scaled linearly in the graph size (stored
+    entries or edges), RHS and distances by the number of blocks, and CG by the
+    column-iterations the GPU run took.
     """
+    import multiprocessing as mp
+
     import numpy as np
 
     import gen
     from oracle import erc as OE
     from oracle import graph as OG
 
+    cpu = host_cpu()
+    procs = procs or min(16, cpu["usable"])
     kb = p.k_block
     nblocks = math.ceil(p.K / kb)
     args = dict(wl.graph_args)
@@ -97,35 +175,132 @@ def cpu_baseline(g, p, wl, iters_total: int, scale_div: int = 25, cg_iters: int 
         gs = g
     f_m = g.m / gs.m
     f_nnz = g.nnz / gs.nnz
+    t_wall0 = time.perf_counter()
     t0 = time.perf_counter()
     L = OG.laplacian(gs)
     eu, ev, _ = OG.canonical_edges(gs)
     t_setup = (time.perf_counter() - t0) * f_m
-    t0 = time.perf_counter()
-    Y = OE.rhs(gs, p.K, 0, kb, p.seed, p.dtype)
-    t_rhs = (time.perf_counter() - t0) * f_nnz * nblocks
-    t0 = time.perf_counter()
-    res = OE.cg_columns(L, p.delta, Y, 1e-300, cg_iters)
-    t_it = (time.perf_counter() - t0) / cg_iters * f_nnz
+    _CPU.update(g=gs, p=p, L=L, iters=cg_iters)
+    bounds = [(kb * k) // procs for k in range(procs + 1)]
+    ranges = [(bounds[k], bounds[k + 1]) for k in range(procs) if bounds[k + 1] > bounds[k]]
+    ctx = mp.get_context("fork")
+    with ctx.Pool(len(ranges), initializer=_cpu_init) as pool:
+        t0 = time.perf_counter()
+        parts = sorted(pool.map(_cpu_rhs, [(a, b - a) for a, b in ranges]))
+        t_rhs_s = time.perf_counter() - t0
+        Y = np.concatenate([y for _, y in parts], axis=1)
+        _CPU["Y"] = Y
+    # a fresh pool so the workers see Y (fork after it is set)
+    with ctx.Pool(len(ranges), initializer=_cpu_init) as pool:
+        t0 = time.perf_counter()
+        zs = sorted(pool.map(_cpu_cg, ranges))
+        t_cg_s = time.perf_counter() - t0
+    Z = np.concatenate([z for _, z in zs], axis=1)
+    t_rhs = t_rhs_s * f_nnz * nblocks
+    t_it = t_cg_s / cg_iters * f_nnz
     t_cg = t_it * iters_total / kb
-    t0 = time.perf_counter()
-    R = OE.edge_distances(res.Z, eu, ev)
-    t_dist = (time.perf_counter() - t0) * f_m * nblocks
-    t0 = time.perf_counter()
-    _, kappa = OE.curvature(gs, R)
-    OE.sampling_probs(gs, kappa, p.eta)
-    t_curv = (time.perf_counter() - t0) * f_m
+    from threadpoolctl import threadpool_limits
+
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        R = OE.edge_distances(Z, eu, ev)
+        t_dist = (time.perf_counter() - t0) * f_m * nblocks
+        t0 = time.perf_counter()
+        _, kappa = OE.curvature(gs, R)
+        OE.sampling_probs(gs, kappa, p.eta)
+        t_curv = (time.perf_counter() - t0) * f_m
+    wall = time.perf_counter() - t_wall0
+    _CPU.clear()
     total = t_setup + t_rhs + t_cg + t_dist + t_curv
-    log(f"cpu baseline: estimated {total:.0f}s for the full workload")
-    sample = (f"oracle (fp64 NumPy/SciPy, one thread) on a 1/{scale_div} instance of the same "
-              f"recipe ({gs.n} nodes, {gs.m} edges), scaled by edges or stored entries: "
-              f"Laplacian assembly {t_setup:.1f}s, RHS x {nblocks} blocks {t_rhs:.1f}s, CG "
-              f"{cg_iters} iterations of a {kb}-column block -> {t_it:.2f}s per iteration at "
-              f"full size x {iters_total} column-iterations / {kb} = {t_cg:.0f}s, edge "
+    log(f"cpu baseline: estimated {total:.0f}s for the full workload on {len(ranges)} processes")
+    sample = (f"oracle (fp64 NumPy/SciPy) on a 1/{scale_div} instance of the same recipe "
+              f"({gs.n} nodes, {gs.m} edges): RHS of one {kb}-column block and {cg_iters} CG "
+              f"iterations of it in {len(ranges)} column ranges on {len(ranges)} processes "
+              f"({t_rhs_s:.1f}s, {t_cg_s:.1f}s measured), Laplacian assembly, edge distances, "
+              f"curvature and sampling on one; scaled by edges or stored entries: assembly "
+              f"{t_setup:.1f}s, RHS x {nblocks} blocks {t_rhs:.1f}s, CG {t_it:.2f}s per "
+              f"block-iteration x {iters_total} column-iterations / {kb} = {t_cg:.0f}s, edge "
               f"distances {t_dist:.1f}s, curvature + sampling {t_curv:.1f}s; estimated full "
               f"run {total:.0f}s")
-    return {"value": g.m / total, "unit": "edges/s", "cores": 1, "kind": "oracle",
-            "sample": sample, "est_seconds": round(total, 1)}
+    return {"value": g.m / total, "unit": "edges/s", "cores": len(ranges), "kind": "oracle",
+            "sample": sample, "est_seconds": round(total, 1),
+            "sample_measured_s": round(wall, 1), "cpu_model": cpu["model"],
+            "nproc": cpu["nproc"], "usable_cpus": cpu["usable"],
+            "processes": len(ranges)}
+
+
+def gather_ceiling(g, kb: int, dtype: str, torch, reps: int = 5, streams=None):
+    """Time the gather probe (erc_probe_gather) replaying index streams over a table of
+    the p block's size (n rows of kb working-precision values): the SpMM's own column
+    indices by default, or the named streams of `streams` (name -> int32 array,
+    footprint in rows).  Median of `reps` launches after one warm-up, HIP events on the
+    stream the probe runs on."""
+    import numpy as np
+
+    from paper_2609_27209_amd import _abi
+
+    row_bytes = kb * elem_bytes(dtype)
+    if streams is None:
+        streams = {"spmm_column_indices": (np.asarray(g.col, np.int32), g.n)}
+    rows_max = max(r for _, r in streams.values())
+    table = torch.empty(rows_max * row_bytes // 4, dtype=torch.float32, device="cuda")
+    table.uniform_()
+    out = {}
+    st = torch.cuda.current_stream()
+    for name, (idx_np, rows) in streams.items():
+        idx = torch.from_numpy(np.ascontiguousarray(idx_np, np.int32)).cuda()
+        res = torch.empty(_abi.erc_probe_out_bytes(idx.numel(), row_bytes) // 4,
+                          dtype=torch.float32, device="cuda")
+        ts = []
+        for r in range(reps + 1):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            _abi.erc_probe_gather(idx.data_ptr(), idx.numel(), table.data_ptr(), rows, row_bytes,
+                                  res.data_ptr(), st.cuda_stream)
+            e1.record(st)
+            torch.cuda.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1))
+        ms = sorted(ts)[len(ts) // 2]
+        gathered = idx.numel() * row_bytes
+        out[name] = {"ms": round(ms, 4), "gathered_bytes": gathered,
+                     "gbs": round(gathered / (ms / 1e3) / 1e9, 1),
+                     "footprint_bytes": rows * row_bytes}
+        log(f"gather probe {name}: {out[name]}")
+        del idx, res
+    del table
+    return out
+
+
+def relabelled_step(g, p, torch, seed: int = 7):
+    """One step (resistance + curvature + sampling probabilities) on a copy of the
+    graph with node ids randomly permuted: the same degree sequence and structure in an
+    order with no hub-first locality.  Times the step and its SpMM launches."""
+    import numpy as np
+
+    import gen
+    import paper_2609_27209_amd as E
+
+    t0 = time.perf_counter()
+    gr = gen.relabel(g, np.random.default_rng(seed).permutation(g.n))
+    t_relabel = time.perf_counter() - t0
+    G = E.Graph(gr.rowptr, gr.col, gr.w, solve_dtype=p.dtype)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed, profile=True)
+    _, kk = G.curvature(R)
+    G.sampling_probs(kk, p.eta)
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    avg = info["ms_spmm"] / max(info["spmm_full"], 1)
+    G.close()
+    del G, R, kk
+    out = {"permutation_seed": seed, "ms_per_step": round(sec * 1e3, 1),
+           "edges_per_s": g.m / sec, "iters_max": info["iters_max"],
+           "spmm_avg_ms": round(avg, 4), "relabel_host_s": round(t_relabel, 1)}
+    log(f"relabelled copy: {out}")
+    return out
 
 
 def subgraph_draw(G, pn, pe, torch, reps: int = 5):
@@ -296,6 +471,38 @@ def block_sweep(name: str, widths):
             "dtype": p.dtype, "rows": rows}
 
 
+def gather_footprints(name: str, torch):
+    """The gather probe's rate for 256-byte-class rows (the workload's p block) on: the
+    SpMM's own column indices; the same indices folded into a footprint of F rows (j mod
+    F), which fits one XCD's L2, all L2s, or the Infinity Cache; the same indices in a
+    random order (no row-order locality); sorted (each row's gathers adjacent: the
+    compulsory bytes from the cache); the hub rows (ids below 131072) and the rest
+    separately; and uniform indices over footprints beyond the Infinity Cache."""
+    import numpy as np
+
+    import gen
+
+    p = gen.CONFIGS[name].params
+    g = gen.make_graph(name, progress=log)
+    kb = padded(p.k_block, p.dtype)
+    col = np.asarray(g.col, np.int32)
+    rng = np.random.default_rng(1)
+    row_bytes = kb * elem_bytes(p.dtype)
+    streams = {"spmm_column_indices": (col, g.n)}
+    for F in (1 << 14, 1 << 17, 1 << 19, 1 << 20):
+        streams[f"folded_{F * row_bytes >> 20}MiB"] = ((col % F).astype(np.int32), F)
+    streams["shuffled"] = (rng.permutation(col), g.n)
+    streams["sorted"] = (np.sort(col), g.n)
+    streams["hub_ids_below_131072"] = (col[col < 131072], g.n)
+    streams["ids_from_131072"] = (col[col >= 131072], g.n)
+    for R in (g.n, 8 << 20, 16 << 20):
+        streams[f"uniform_{R * row_bytes >> 20}MiB"] = (
+            rng.integers(0, R, size=col.size, dtype=np.int32), R)
+    res = gather_ceiling(g, kb, p.dtype, torch, streams=streams)
+    return {"table": "gather_ceiling", "workload": name, "row_bytes": row_bytes,
+            "indices": int(col.size), "kernel": "k_probe_gather", "rows": res}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -316,6 +523,14 @@ def main() -> int:
                          "these block widths")
     ap.add_argument("--no-draw", action="store_true",
                     help="skip the subgraph-draw measurement after the timed steps")
+    ap.add_argument("--no-relabel", action="store_true",
+                    help="skip the step on a randomly relabelled copy of the graph")
+    ap.add_argument("--no-gather-probe", action="store_true",
+                    help="skip timing the gather probe on the SpMM's column indices")
+    ap.add_argument("--gather-ceiling", action="store_true",
+                    help="instead of the benchmark line: one line with the gather probe's "
+                         "rate on the --config workload's column indices and on index "
+                         "streams with controlled footprints")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this size 3 times (a plain "
                          "copy kernel of known size, to calibrate HBM byte counters)")
@@ -342,6 +557,9 @@ def main() -> int:
     if args.block_sweep:
         widths = [int(b) for b in args.block_sweep.split(",")]
         print(json.dumps(block_sweep(args.config, widths)), flush=True)
+        return 0
+    if args.gather_ceiling:
+        print(json.dumps(gather_footprints(args.config, torch)), flush=True)
         return 0
     wl = gen.CONFIGS[args.config]
     p = wl.params
@@ -394,6 +612,7 @@ def main() -> int:
     spmm_n = sum(i["spmm_timed"] for i in infos)
     avg_spmm_ms = spmm_ms / max(spmm_full, 1)
     bytes_launch = spmm_bytes_per_launch(g, kb, p.dtype)
+    fused_launch = spmm_fused_bytes_per_launch(g, kb, p.dtype)
     achieved = bytes_launch / (avg_spmm_ms / 1000.0) / 1e9
     traffic = None
     if (MEASURED_TRAFFIC["workload"] == args.config
@@ -403,15 +622,38 @@ def main() -> int:
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": "k_spmm", "bytes_per_launch": bytes_launch,
                 "avg_launch_ms": round(avg_spmm_ms, 4), "launches_full": spmm_full,
-                "launches_timed": spmm_n}
+                "launches_timed": spmm_n,
+                "fused_bytes_per_launch": fused_launch,
+                "achieved_on_fused_bytes": round(fused_launch / (avg_spmm_ms / 1e3) / 1e9, 1)}
     if traffic is not None:
         tb = traffic / (avg_spmm_ms / 1000.0) / 1e9
-        roofline["traffic_gbs"] = round(tb, 1)
-        roofline["traffic_frac"] = round(tb / PEAK_HBM_GBS, 4)
+        # L2-to-fabric rate: requests served by the Infinity Cache count as well as HBM
+        roofline["fabric_gbs"] = round(tb, 1)
+        roofline["fabric_vs_hbm_peak"] = round(tb / PEAK_HBM_GBS, 4)
+        roofline["traffic_counted"] = "FETCH_SIZE + WRITE_SIZE: L2-to-fabric bytes (HBM and Infinity Cache)"
     iters_total = infos[-1]["iters_total"]
+    # the whole CG inner loop (SpMM + finishing step + update) on the model bytes of an
+    # iteration, over the timed steps
+    ib = iteration_bytes(g, kb, p.dtype)
+    ms_cg = sum(i["ms_cg"] for i in infos)
+    loop_gbs = ib * spmm_full / (ms_cg / 1e3) / 1e9
+    roofline["inner_loop"] = {"bytes_per_iteration": ib, "iterations": spmm_full,
+                              "ms": round(ms_cg, 1), "achieved": round(loop_gbs, 1),
+                              "frac": round(loop_gbs / PEAK_HBM_GBS, 4)}
+    if not args.no_gather_probe:
+        gc = gather_ceiling(g, kb, p.dtype, torch)["spmm_column_indices"]
+        roofline["gather_ceiling"] = dict(gc, kernel="k_probe_gather",
+                                          spmm_time_over_probe=round(avg_spmm_ms / gc["ms"], 3))
 
     draw = None if args.no_draw else subgraph_draw(G, last["pn"], last["pe"], torch)
     variants = None if args.no_variants else {"jacobi": jacobi_variant(G, g, p, last["R"], torch)}
+    relabelled = None
+    if not args.no_relabel:
+        G.close()
+        del G
+        last.clear()
+        torch.cuda.empty_cache()
+        relabelled = relabelled_step(g, p, torch)
 
     if args.copy_probe_mib > 0:
         nb = args.copy_probe_mib << 20
@@ -426,15 +668,11 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         try:
-            t0 = time.perf_counter()
-            from threadpoolctl import threadpool_limits
-
-            with threadpool_limits(limits=1):  # the oracle runs on one host thread
-                cpu = cpu_baseline(g, p, wl, iters_total, args.cpu_scale)
-            cpu["sample_wall_s"] = round(time.perf_counter() - t0, 1)
+            cpu = cpu_baseline(g, p, wl, iters_total, args.cpu_scale)
         except MemoryError as exc:  # pragma: no cover - host-dependent
             log(f"cpu baseline skipped: {exc}")
 
+    summ = g.summary()
     line = {
         "metric": "CG SpMM achieved HBM GB/s (% peak) + curvature edges/sec end-to-end",
         "value": value,
@@ -451,12 +689,15 @@ def main() -> int:
         "dtype": "f32" if p.dtype == "f32" else "f64",
         "data": "synthetic",
         "config": {"workload": args.config, "description": wl.description, "n": g.n, "m": g.m,
+                   "deg_min": summ["deg_min"], "deg_median": summ["deg_median"],
+                   "deg_max": summ["deg_max"], "components": gen.component_count(g),
                    "K": p.K, "k_block": p.k_block, "delta": p.delta, "tol": p.tol,
                    "seed": p.seed, "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "subgraph_draw": draw,
         "variants": variants,
+        "relabelled_copy": relabelled,
         "solve": {"iters_max": infos[-1]["iters_max"], "iters_total": iters_total,
                   "max_final_relres": infos[-1]["max_final_relres"],
                   "ms_rhs": infos[-1]["ms_rhs"], "ms_cg": infos[-1]["ms_cg"],

@@ -19,5 +19,7 @@ from .graphs import (  # noqa: F401
     erdos_renyi,
     sbm,
     chung_lu,
+    component_count,
+    relabel,
 )
 from .configs import CONFIGS, SolveParams, Workload, make_graph, get_workload  # noqa: F401

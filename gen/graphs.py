@@ -17,7 +17,7 @@ import numpy as np
 __all__ = [
     "CSRGraph", "from_edges", "complete_graph", "cycle_graph", "path_graph",
     "star_graph", "complete_bipartite", "random_tree", "barbell_graph",
-    "erdos_renyi", "sbm", "chung_lu",
+    "erdos_renyi", "sbm", "chung_lu", "component_count", "relabel",
 ]
 
 
@@ -263,6 +263,31 @@ def largest_component(g: CSRGraph) -> CSRGraph:
     v = newid[g.col[upper]]
     w = None if g.w is None else g.w[upper]
     return from_edges(int(keep.sum()), u, v, w, sorted_unique=True)
+
+
+def component_count(g: CSRGraph) -> int:
+    """Number of connected components (isolated nodes count as components)."""
+    import scipy.sparse as sp
+    from scipy.sparse.csgraph import connected_components
+
+    A = sp.csr_matrix((np.ones(g.nnz, dtype=np.int8), g.col, g.rowptr), shape=(g.n, g.n))
+    return int(connected_components(A, directed=False)[0])
+
+
+def relabel(g: CSRGraph, perm) -> CSRGraph:
+    """The same graph with node i renamed perm[i] (perm a permutation of 0..n-1); each
+    stored entry keeps its weight, rows and their columns come out sorted."""
+    perm = np.asarray(perm, dtype=np.int64)
+    if perm.shape != (g.n,) or not np.array_equal(np.sort(perm), np.arange(g.n)):
+        raise ValueError("perm must be a permutation of 0..n-1")
+    rows = perm[np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.rowptr))]
+    cols = perm[np.asarray(g.col, dtype=np.int64)]
+    order = np.argsort(rows * g.n + cols, kind="stable")
+    rowptr = np.zeros(g.n + 1, dtype=np.int64)
+    np.cumsum(np.bincount(rows, minlength=g.n), out=rowptr[1:])
+    col = cols[order].astype(np.int32)
+    w = None if g.w is None else np.asarray(g.w)[order]
+    return CSRGraph(g.n, rowptr, col, w)
 
 
 def chung_lu(n: int, gamma: float, i0: float, m_target: int, seed: int,

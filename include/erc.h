@@ -90,6 +90,12 @@ typedef struct {
  * widely spread degrees it needs far fewer iterations.  A variant, not the paper's
  * method: results equal the plain solve only up to the CG truncation error. */
 #define ERC_JACOBI 4u
+/* Enqueue every CG iteration as separate kernel launches.  By default each group of
+ * check_every iterations is captured once into a HIP graph (on a stream the handle
+ * owns) and replayed on the caller's stream, which removes most of the per-launch
+ * overhead on small graphs; the kernels, their order and the results are the same.
+ * ERC_PROFILE_SPMM implies this flag (its events sit between the launches). */
+#define ERC_NO_GRAPH 8u
 
 /* Parameters of one resistance sweep (Algorithm 1, Require line).
  *  K_total     total projection dimension K; the JL scale is 1/sqrt(K_total) even when
@@ -106,7 +112,7 @@ typedef struct {
  *  check_every iterations enqueued between host convergence polls (0 = default 16);
  *              results do not depend on it
  *  seed        projection seed
- *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI, or 0 */
+ *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH, or 0 */
 typedef struct {
   int32_t K_total;
   int32_t k_block;
@@ -201,7 +207,8 @@ erc_status erc_curvature(erc_handle h, const double* R_dev, double* p_dev, doubl
  * when every q_u is 0 (Eq. 7).  Edge probabilities (device, m fp64):
  * q_e = sqrt(max(2 kappa_max - kappa_e, 0)) + 1 divided by its sum (Eq. 8).
  * eta > 0.  scratch_dev is device memory of >= erc_sampling_scratch_bytes bytes.
- * Asynchronous. */
+ * Blocks until the stream has drained.  ERC_E_NUMERIC, with every probability written
+ * as NaN, when some kappa_e is NaN or infinite. */
 erc_status erc_sampling_scratch_bytes(erc_handle h, size_t* bytes);
 erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
                               void* scratch_dev, size_t scratch_bytes,
@@ -249,6 +256,22 @@ erc_status erc_subgraph(erc_handle h, erc_items items, const int64_t* idx_dev, i
 
 const char* erc_status_string(erc_status s);
 const char* erc_last_error(void);
+
+/* ---- measurement hook (memory-system probe for the roofline of gather kernels) ----- */
+
+/* Rows of row_bytes bytes that erc_probe_gather stores for `count` indices. */
+erc_status erc_probe_out_bytes(int64_t count, int32_t row_bytes, size_t* bytes);
+
+/* For every k in [0, count): load row idx_dev[k] of table_dev (device, rows x row_bytes
+ * bytes, row-major, 16-byte aligned) with the SpMM's gather access pattern (row_bytes/16
+ * lanes, one 16-byte load each, eight rows in flight per lane group) and sum the rows
+ * of each contiguous range of indices into one row of out_dev (device,
+ * erc_probe_out_bytes).  Indices outside [0, rows) read row 0.  row_bytes: a power of
+ * two in 64..1024.  Replaying the SpMM's own column indices over a table of the
+ * p block's size times its gathers alone; no part of the method is computed.
+ * Asynchronous. */
+erc_status erc_probe_gather(const int32_t* idx_dev, int64_t count, const void* table_dev,
+                            int64_t rows, int32_t row_bytes, void* out_dev, void* stream);
 
 /* ---- test hooks (same conventions; used by the parity tests) ---------------------- */
 

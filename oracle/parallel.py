@@ -11,6 +11,7 @@ from __future__ import annotations
 import multiprocessing as mp
 import os
 import tempfile
+import time
 
 import numpy as np
 
@@ -23,13 +24,44 @@ _L = None
 
 def _work(args):
     c0, c1, prm, path = args
+    t0 = time.time()
     R, info = erc.resistance(_G, prm["K"], prm["k_block"], prm["delta"], prm["tol"],
                              prm["max_iter"], prm["seed"], prm["dtype"], c0, c1, L=_L,
                              precond=prm["precond"])
-    np.save(path, R)
     iters = np.concatenate(info.iters) if info.iters else np.zeros(0, np.int64)
     conv = np.concatenate(info.converged) if info.converged else np.zeros(0, bool)
+    np.savez(path, R=R, iters=iters, conv=conv, seconds=time.time() - t0)
     return c0, c1, iters, conv
+
+
+def solve_chunks(g, chunks, paths, K, k_block, delta, tol, max_iter, seed, dtype="f64",
+                 procs=None, progress=None, precond="none"):
+    """Solve each column range chunks[i] = (c0, c1) in a pool of ``procs`` processes and
+    write its R, iteration counts and convergence flags to paths[i] (``.npz``).
+
+    Chunks are independent and may come from several disjoint ranges; each file holds
+    exactly what ``erc.resistance`` returns for that range alone.
+    """
+    global _G, _L
+    assert len(chunks) == len(paths)
+    if not chunks:
+        return
+    GR.check_graph(g)
+    _G = g
+    _L = GR.laplacian(g)
+    prm = dict(K=K, k_block=k_block, delta=delta, tol=tol, max_iter=max_iter, seed=seed,
+               dtype=dtype, precond=precond)
+    jobs = [(c0, c1, prm, path) for (c0, c1), path in zip(chunks, paths)]
+    procs = max(1, min(procs or min(8, os.cpu_count() or 1), len(jobs)))
+    try:
+        ctx = mp.get_context("fork")
+        with ctx.Pool(procs) as pool:
+            for res in pool.imap_unordered(_work, jobs):
+                if progress:
+                    progress(f"oracle columns [{res[0]}, {res[1]}) done")
+    finally:
+        _G = None
+        _L = None
 
 
 def resistance_parallel(g, K, k_block, delta, tol, max_iter, seed, dtype="f64", col_begin=0,
@@ -39,33 +71,21 @@ def resistance_parallel(g, K, k_block, delta, tol, max_iter, seed, dtype="f64", 
     Returns (R, iters, converged) with per-column iteration counts and flags in column
     order.
     """
-    global _G, _L
     col_end = K if col_end is None else col_end
     procs = procs or min(8, os.cpu_count() or 1)
     ncol = col_end - col_begin
     procs = max(1, min(procs, ncol))
     bounds = [col_begin + (ncol * k) // procs for k in range(procs + 1)]
-    GR.check_graph(g)
-    _G = g
-    _L = GR.laplacian(g)
-    prm = dict(K=K, k_block=k_block, delta=delta, tol=tol, max_iter=max_iter, seed=seed,
-               dtype=dtype, precond=precond)
+    chunks = [(bounds[k], bounds[k + 1]) for k in range(procs)]
     with tempfile.TemporaryDirectory(prefix="erc_oracle_") as tmp:
-        jobs = [(bounds[k], bounds[k + 1], prm, os.path.join(tmp, f"R{k}.npy"))
-                for k in range(procs)]
-        ctx = mp.get_context("fork")
-        with ctx.Pool(procs) as pool:
-            results = []
-            for res in pool.imap_unordered(_work, jobs):
-                results.append(res)
-                if progress:
-                    progress(f"oracle columns [{res[0]}, {res[1]}) done")
-        results.sort(key=lambda r: r[0])
+        paths = [os.path.join(tmp, f"R{k}.npz") for k in range(procs)]
+        solve_chunks(g, chunks, paths, K, k_block, delta, tol, max_iter, seed, dtype,
+                     procs=procs, progress=progress, precond=precond)
         R = np.zeros(g.m)
-        for k in range(procs):
-            R += np.load(jobs[k][3])
-    iters = np.concatenate([r[2] for r in results])
-    conv = np.concatenate([r[3] for r in results])
-    _G = None
-    _L = None
-    return R, iters, conv
+        iters, conv = [], []
+        for path in paths:
+            with np.load(path) as f:
+                R += f["R"]
+                iters.append(f["iters"])
+                conv.append(f["conv"])
+    return R, np.concatenate(iters), np.concatenate(conv)

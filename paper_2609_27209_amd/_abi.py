@@ -30,6 +30,7 @@ ERC_EDGES = 1
 ERC_ACCUMULATE = 1
 ERC_PROFILE_SPMM = 2
 ERC_JACOBI = 4
+ERC_NO_GRAPH = 8
 
 
 class erc_graph_desc(ctypes.Structure):
@@ -98,6 +99,8 @@ _SIGNATURES = {
     "erc_subgraph_scratch_bytes": [c_void_p, POINTER(c_size_t)],
     "erc_subgraph": [c_void_p, c_int, c_void_p, c_int64, c_void_p, c_size_t, c_void_p, c_void_p,
                      c_void_p, c_void_p, POINTER(c_int64), c_void_p],
+    "erc_probe_out_bytes": [c_int64, c_int32, POINTER(c_size_t)],
+    "erc_probe_gather": [c_void_p, c_int64, c_void_p, c_int64, c_int32, c_void_p, c_void_p],
     "erc_status_string": [c_int],
     "erc_last_error": [],
     "erc_debug_check_plan": [POINTER(erc_graph_desc)],
@@ -215,6 +218,18 @@ def erc_sampling_probs(h: int, kappa_dev: int, eta: float, scratch: int, scratch
     _check(load().erc_sampling_probs(c_void_p(h), c_void_p(kappa_dev), eta, c_void_p(scratch),
                                      scratch_bytes, c_void_p(pn_dev), c_void_p(pe_dev),
                                      c_void_p(stream)))
+
+
+def erc_probe_out_bytes(count: int, row_bytes: int) -> int:
+    b = c_size_t(0)
+    _check(load().erc_probe_out_bytes(count, row_bytes, byref(b)))
+    return b.value
+
+
+def erc_probe_gather(idx_dev: int, count: int, table_dev: int, rows: int, row_bytes: int,
+                     out_dev: int, stream: int) -> None:
+    _check(load().erc_probe_gather(c_void_p(idx_dev), count, c_void_p(table_dev), rows, row_bytes,
+                                   c_void_p(out_dev), c_void_p(stream)))
 
 
 def erc_draw_scratch_bytes(h: int, items: int) -> int:

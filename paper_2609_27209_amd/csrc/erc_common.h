@@ -55,6 +55,7 @@ struct DevGraph {
   const int64_t* task_beg;   // CSR range of the task
   const int64_t* task_end;
   int32_t nmega;
+  const int32_t* mega_row;     // row of each multi-chunk row
   const int32_t* mega_nchunk;
   const int32_t* mega_chunk0;  // first chunk slot of each multi-chunk row
   int32_t nchunk_slots;
@@ -105,7 +106,6 @@ struct Work {
   void* q;
   void* chunkbuf;    // nchunk_slots x kb partial sums of multi-chunk rows
   double* mega_dots; // nmega x 3 x kb compensated (s, c) pairs
-  uint32_t* mega_tick;  // nmega counters
   ColState cs;
   double* part;      // block partials of the SpMM / RHS launch: grid x 3 x kb pairs
   double* part_u;    // block partials of the update launch: grid_upd x kb pairs
@@ -147,6 +147,11 @@ struct SampleWork {
 };
 hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,
                            const SampleWork& sw, double* pn, double* pe, hipStream_t s);
+
+// Gather probe (erc_probe.hip): rows of sums it stores for `count` indices, and launch.
+int64_t probe_out_rows(int64_t count);
+hipError_t launch_probe_gather(const int32_t* idx, int64_t count, const void* table, int64_t rows,
+                               int row_bytes, void* out, hipStream_t s);
 
 // Tree sizing helpers (host).
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

@@ -119,7 +119,7 @@ Shape make_shape(int64_t n, int64_t nnz) {
 // Byte layout of the graph buffer.
 struct GraphLayout {
   int64_t rowptr, col, w, eid, sw, ubase, deg, light, wave_lo, task_row, task_mega, task_chunk,
-      task_beg, task_end, mega_nchunk, mega_chunk0, piece_row, piece_beg, piece_end, total;
+      task_beg, task_end, mega_row, mega_nchunk, mega_chunk0, piece_row, piece_beg, piece_end, total;
 };
 
 GraphLayout graph_layout(const Shape& s, bool weighted, erc_dtype dt) {
@@ -144,6 +144,7 @@ GraphLayout graph_layout(const Shape& s, bool weighted, erc_dtype dt) {
   L.task_chunk = take(s.ntask_max * 4);
   L.task_beg = take(s.ntask_max * 8);
   L.task_end = take(s.ntask_max * 8);
+  L.mega_row = take(s.nmega_max * 4);
   L.mega_nchunk = take(s.nmega_max * 4);
   L.mega_chunk0 = take(s.nmega_max * 4);
   L.piece_row = take(s.npiece_max * 4);
@@ -354,7 +355,7 @@ struct Plan {
   std::vector<int32_t> light, wave_lo;
   std::vector<int32_t> task_row, task_mega, task_chunk;
   std::vector<int64_t> task_beg, task_end;
-  std::vector<int32_t> mega_nchunk, mega_chunk0;
+  std::vector<int32_t> mega_row, mega_nchunk, mega_chunk0;
   int32_t nslot = 0;
   std::vector<int32_t> piece_row;
   std::vector<int64_t> piece_beg, piece_end;
@@ -379,6 +380,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
       tasks.push_back({i, -1, 0, b, e});
     } else {
       const int32_t mh = static_cast<int32_t>(P->mega_nchunk.size());
+      P->mega_row.push_back(i);
       P->mega_nchunk.push_back(static_cast<int32_t>(nch));
       P->mega_chunk0.push_back(P->nslot);
       P->nslot += static_cast<int32_t>(nch);
@@ -447,7 +449,7 @@ void build_plan(const erc_graph_desc* d, const Canon& c, const Shape& s, Plan* P
 
 // Workspace layout for a padded block width.
 struct WorkLayout {
-  int64_t z, r, p, q, chunkbuf, mega_dots, mega_tick, rho, rr, rho0, thr, alpha, beta, active,
+  int64_t z, r, p, q, chunkbuf, mega_dots, rho, rr, rho0, thr, alpha, beta, active,
       iters, status, n_active, upd_pending, pred_done, nspmm, fin_ctr, one, part, part_u, lvl0, lvl1, lvl2, tick, out, minv,
       total;
   int grid_rhs, grid_upd, grid_ed, grid_tree;
@@ -471,14 +473,27 @@ struct erc_graph_s {
   Shape shape{};
   DevGraph dg{};
   int32_t* pinned = nullptr;  // host poll slots and per-column readback
-  hipEvent_t ev[6] = {};
+  // [0..3] block phases, [4..5] poll groups, [6..7] whole erc_resistance call
+  hipEvent_t ev[8] = {};
   std::vector<hipEvent_t> prof;  // SpMM timing pairs: [slot][launch][begin/end]
   int prof_check = 0;
+  // one group of CG iterations captured as a HIP graph, replayed on the caller's stream;
+  // the key names everything the captured kernel arguments depend on
+  hipStream_t cap = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  struct GroupKey {
+    const void* ws = nullptr;
+    int kb = 0, pc = 0, nb = 0;
+    double delta = 0.0;
+  } gkey;
 };
 
 namespace {
 
 constexpr int kPinnedInts = 4096;
+// pinned slot (8-byte aligned) of the sampling call's non-finite-curvature flag, past the
+// per-column readback of the widest block (8 + 4 * 256 + 4 * 256 ints)
+constexpr int kPinSampleFlag = 4064;
 
 WorkLayout work_layout(const erc_graph_s* h, int kb) {
   WorkLayout L{};
@@ -502,7 +517,6 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.q = take(vecb);
   L.chunkbuf = take(static_cast<int64_t>(h->dg.nchunk_slots) * kb * s);
   L.mega_dots = take(static_cast<int64_t>(h->dg.nmega) * 3 * kb * 16);
-  L.mega_tick = take(static_cast<int64_t>(h->dg.nmega) * 4);
   L.rho = take(kb * 8);
   L.rr = take(kb * 8);
   L.rho0 = take(kb * 8);
@@ -542,7 +556,6 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
   w.q = b + L.q;
   w.chunkbuf = b + L.chunkbuf;
   w.mega_dots = reinterpret_cast<double*>(b + L.mega_dots);
-  w.mega_tick = reinterpret_cast<uint32_t*>(b + L.mega_tick);
   w.cs.rho = reinterpret_cast<double*>(b + L.rho);
   w.cs.rr = reinterpret_cast<double*>(b + L.rr);
   w.cs.rho0 = reinterpret_cast<double*>(b + L.rho0);
@@ -579,7 +592,6 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
 // records no memset node).
 erc_status prepare_work(const erc_graph_s* h, const Work& w, const WorkLayout& L, hipStream_t s) {
   ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(kMaxTreeGrid), s));
-  ERC_HIP(launch_fill_u32(w.mega_tick, 0u, h->dg.nmega, s));
   ERC_HIP(launch_fill_u32(w.cs.fin_cnt, 0u, 3, s));
   ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.one), 1u, 1, s));
   return ERC_OK;
@@ -604,7 +616,7 @@ erc_status check_params(const erc_graph_s* h, const erc_solve_params* p) {
   if (!(p->tol > 0.0 && p->tol < 1.0)) return fail(ERC_E_INVALID_ARG, "tol must be in (0, 1)");
   if (p->max_iter < 1) return fail(ERC_E_INVALID_ARG, "max_iter must be >= 1");
   if (p->check_every < 0) return fail(ERC_E_INVALID_ARG, "check_every must be >= 0");
-  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI)) != 0u)
+  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH)) != 0u)
     return fail(ERC_E_INVALID_ARG, "unknown flag");
   return ERC_OK;
 }
@@ -639,6 +651,51 @@ erc_status read_prof(erc_graph_s* h, int slot, int count, BlockStats* st) {
   return ERC_OK;
 }
 
+// One CG iteration: SpMM (+ split-row finish), finishing step, update, and the early
+// stopping test that runs only when every column is predicted to stop.
+hipError_t enqueue_iteration(const erc_graph_s* h, const Work& w, double delta, hipStream_t s) {
+  hipError_t e = launch_spmm(h->dg, w, h->dt, delta, w.p, w.r, w.q, w.cs.n_active, s);
+  if (e == hipSuccess) e = launch_fin_iter(h->dg, w, 0, s);
+  if (e == hipSuccess) e = launch_update(h->dg, w, h->dt, s);
+  // the exact stopping test, only when every column is predicted to stop: saves the
+  // SpMM that would otherwise run after the last update
+  if (e == hipSuccess) e = launch_fin_iter(h->dg, w, 2, s);
+  return e;
+}
+
+// Capture nb iterations into the handle's graph unless the cached one has the same
+// kernel arguments (same workspace, width, variant and shift).
+erc_status ensure_group_graph(erc_graph_s* h, const Work& w, double delta, int nb) {
+  erc_graph_s::GroupKey k;
+  k.ws = w.z;
+  k.kb = w.kb;
+  k.pc = w.pc;
+  k.nb = nb;
+  k.delta = delta;
+  const erc_graph_s::GroupKey& o = h->gkey;
+  if (h->gexec != nullptr && o.ws == k.ws && o.kb == k.kb && o.pc == k.pc && o.nb == k.nb &&
+      o.delta == k.delta)
+    return ERC_OK;
+  if (h->gexec != nullptr) {
+    (void)hipGraphExecDestroy(h->gexec);
+    h->gexec = nullptr;
+  }
+  ERC_HIP(hipStreamBeginCapture(h->cap, hipStreamCaptureModeThreadLocal));
+  hipError_t e = hipSuccess;
+  for (int j = 0; j < nb && e == hipSuccess; ++j) e = enqueue_iteration(h, w, delta, h->cap);
+  hipGraph_t g = nullptr;
+  const hipError_t ee = hipStreamEndCapture(h->cap, &g);
+  if (e == hipSuccess) e = ee;
+  hipGraphExec_t x = nullptr;
+  if (e == hipSuccess) e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+  if (g != nullptr) (void)hipGraphDestroy(g);
+  if (e != hipSuccess)
+    return fail(ERC_E_DEVICE, std::string("CG group capture: ") + hipGetErrorString(e));
+  h->gexec = x;
+  h->gkey = k;
+  return ERC_OK;
+}
+
 // One column block: right-hand sides, CG to tol or max_iter, then (if R != nullptr)
 // the edge-distance accumulation.  Ends with the stream drained.
 erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w, int col0, int nc,
@@ -652,6 +709,7 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
   ERC_HIP(hipEventRecord(h->ev[1], s));
   const int check = p->check_every > 0 ? p->check_every : kDefaultCheck;
   const bool prof = (p->flags & ERC_PROFILE_SPMM) != 0u;
+  const bool graph = !prof && (p->flags & ERC_NO_GRAPH) == 0u;
   if (prof) {
     erc_status pst = ensure_prof_events(h, check);
     if (pst != ERC_OK) return pst;
@@ -663,16 +721,25 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
   while (!stop && done < p->max_iter) {
     const int nb = std::min(check, p->max_iter - done);
     slot ^= 1;
-    for (int j = 0; j < nb; ++j) {
-      hipEvent_t* pr = prof ? &h->prof[(static_cast<size_t>(slot) * h->prof_check + j) * 2] : nullptr;
-      if (prof) ERC_HIP(hipEventRecord(pr[0], s));
-      ERC_HIP(launch_spmm(h->dg, w, h->dt, p->delta, w.p, w.r, w.q, w.cs.n_active, s));
-      if (prof) ERC_HIP(hipEventRecord(pr[1], s));
-      ERC_HIP(launch_fin_iter(h->dg, w, 0, s));
-      ERC_HIP(launch_update(h->dg, w, h->dt, s));
-      // the exact stopping test, only when every column is predicted to stop: saves
-      // the SpMM that would otherwise run after the last update
-      ERC_HIP(launch_fin_iter(h->dg, w, 2, s));
+    if (graph && nb == check) {
+      erc_status gst = ensure_group_graph(h, w, p->delta, nb);
+      if (gst != ERC_OK) return gst;
+      ERC_HIP(hipGraphLaunch(h->gexec, s));
+    } else {
+      for (int j = 0; j < nb; ++j) {
+        hipEvent_t* pr = prof ? &h->prof[(static_cast<size_t>(slot) * h->prof_check + j) * 2] : nullptr;
+        if (prof) {
+          // the SpMM alone between the events (its split-row finish follows it)
+          ERC_HIP(hipEventRecord(pr[0], s));
+          ERC_HIP(launch_spmm(h->dg, w, h->dt, p->delta, w.p, w.r, w.q, w.cs.n_active, s));
+          ERC_HIP(hipEventRecord(pr[1], s));
+          ERC_HIP(launch_fin_iter(h->dg, w, 0, s));
+          ERC_HIP(launch_update(h->dg, w, h->dt, s));
+          ERC_HIP(launch_fin_iter(h->dg, w, 2, s));
+        } else {
+          ERC_HIP(enqueue_iteration(h, w, p->delta, s));
+        }
+      }
     }
     group_count[slot] = nb;
     done += nb;
@@ -847,6 +914,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
       if (h->pinned) (void)hipHostFree(h->pinned);
       for (auto& ev : h->ev)
         if (ev) (void)hipEventDestroy(ev);
+      if (h->cap) (void)hipStreamDestroy(h->cap);
       delete h;
       return e;
     };
@@ -856,6 +924,9 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
       return cleanup(fail(ERC_E_DEVICE, "hipHostMalloc failed"));
     for (auto& ev : h->ev)
       if (hipEventCreate(&ev) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipEventCreate failed"));
+    // default priority (no priority argument): the stream only records graph captures
+    if (hipStreamCreateWithFlags(&h->cap, hipStreamNonBlocking) != hipSuccess)
+      return cleanup(fail(ERC_E_DEVICE, "hipStreamCreateWithFlags failed"));
     char* base = static_cast<char*>(dev_mem);
     hipStream_t hs = static_cast<hipStream_t>(stream);
     auto up = [&](int64_t off, const void* src, int64_t nbytes) -> hipError_t {
@@ -885,6 +956,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
     chk(up(L.task_beg, P.task_beg.data(), nt * 8));
     chk(up(L.task_end, P.task_end.data(), nt * 8));
     const int64_t nm = static_cast<int64_t>(P.mega_nchunk.size());
+    chk(up(L.mega_row, P.mega_row.data(), nm * 4));
     chk(up(L.mega_nchunk, P.mega_nchunk.data(), nm * 4));
     chk(up(L.mega_chunk0, P.mega_chunk0.data(), nm * 4));
     const int64_t np = static_cast<int64_t>(P.piece_row.size());
@@ -917,6 +989,7 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
     g.task_beg = reinterpret_cast<const int64_t*>(base + L.task_beg);
     g.task_end = reinterpret_cast<const int64_t*>(base + L.task_end);
     g.nmega = static_cast<int32_t>(nm);
+    g.mega_row = reinterpret_cast<const int32_t*>(base + L.mega_row);
     g.mega_nchunk = reinterpret_cast<const int32_t*>(base + L.mega_nchunk);
     g.mega_chunk0 = reinterpret_cast<const int32_t*>(base + L.mega_chunk0);
     g.nchunk_slots = P.nslot;
@@ -968,6 +1041,8 @@ erc_status erc_destroy(erc_handle h) {
       if (ev) (void)hipEventDestroy(ev);
     for (auto& ev : h->prof)
       if (ev) (void)hipEventDestroy(ev);
+    if (h->gexec) (void)hipGraphExecDestroy(h->gexec);
+    if (h->cap) (void)hipStreamDestroy(h->cap);
     delete h;
     return ERC_OK;
   });
@@ -1002,9 +1077,7 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
     st = prepare_work(h, w, L, s);
     if (st != ERC_OK) return st;
-    hipEvent_t t0 = nullptr, t1 = nullptr;
-    ERC_HIP(hipEventCreate(&t0));
-    ERC_HIP(hipEventCreate(&t1));
+    hipEvent_t t0 = h->ev[6], t1 = h->ev[7];
     ERC_HIP(hipEventRecord(t0, s));
     BlockStats bs;
     int blocks = 0;
@@ -1012,11 +1085,7 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
       const int nc = std::min(params->k_block, params->col_end - c0);
       const int acc = (c0 == params->col_begin && !(params->flags & ERC_ACCUMULATE)) ? 0 : 1;
       st = solve_block(h, params, w, c0, nc, h->m > 0 ? R_dev : nullptr, acc, nullptr, &bs, s);
-      if (st != ERC_OK) {
-        (void)hipEventDestroy(t0);
-        (void)hipEventDestroy(t1);
-        return st;
-      }
+      if (st != ERC_OK) return st;
       ++blocks;
     }
     int64_t bad = 0;
@@ -1034,8 +1103,6 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     }
     float total = 0.0f;
     (void)hipEventElapsedTime(&total, t0, t1);  // timing only: 0 if unavailable
-    (void)hipEventDestroy(t0);
-    (void)hipEventDestroy(t1);
     if (info) {
       info->blocks = blocks;
       info->iters_max = bs.iters_max;
@@ -1153,6 +1220,12 @@ erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
     ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
     ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
     ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
+    // the minimum/maximum pass flags a NaN or infinite kappa (the probabilities are then
+    // written as NaN); the flag comes back to the host so the call can report it
+    double* flag = reinterpret_cast<double*>(h->pinned + kPinSampleFlag);
+    ERC_HIP(hipMemcpyAsync(flag, sw.totals + 4, sizeof(double), hipMemcpyDeviceToHost, s));
+    ERC_HIP(hipStreamSynchronize(s));
+    if (*flag != 0.0) return fail(ERC_E_NUMERIC, "curvature contains NaN or infinite values");
     return ERC_OK;
   });
 }
@@ -1298,6 +1371,35 @@ erc_status erc_subgraph(erc_handle h, erc_items items, const int64_t* idx_dev, i
   });
 }
 
+erc_status erc_probe_out_bytes(int64_t count, int32_t row_bytes, size_t* bytes) {
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (bytes == nullptr) return fail(ERC_E_INVALID_ARG, "bytes is NULL");
+    if (count < 0) return fail(ERC_E_INVALID_ARG, "count must be >= 0");
+    if (row_bytes < 64 || row_bytes > 1024 || (row_bytes & (row_bytes - 1)) != 0)
+      return fail(ERC_E_INVALID_ARG, "row_bytes must be a power of two in 64..1024");
+    *bytes = static_cast<size_t>(std::max<int64_t>(1, probe_out_rows(count)) * row_bytes);
+    return ERC_OK;
+  });
+}
+
+erc_status erc_probe_gather(const int32_t* idx_dev, int64_t count, const void* table_dev,
+                            int64_t rows, int32_t row_bytes, void* out_dev, void* stream) {
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (count < 0 || rows < 1) return fail(ERC_E_INVALID_ARG, "count must be >= 0 and rows >= 1");
+    if (row_bytes < 64 || row_bytes > 1024 || (row_bytes & (row_bytes - 1)) != 0)
+      return fail(ERC_E_INVALID_ARG, "row_bytes must be a power of two in 64..1024");
+    if (count > 0 && (idx_dev == nullptr || table_dev == nullptr || out_dev == nullptr))
+      return fail(ERC_E_INVALID_ARG, "NULL buffer");
+    if (reinterpret_cast<uintptr_t>(table_dev) % 16 != 0 || reinterpret_cast<uintptr_t>(out_dev) % 16 != 0)
+      return fail(ERC_E_INVALID_ARG, "table and output must be 16-byte aligned");
+    ERC_HIP(launch_probe_gather(idx_dev, count, table_dev, rows, row_bytes, out_dev,
+                                static_cast<hipStream_t>(stream)));
+    return ERC_OK;
+  });
+}
+
 erc_status erc_debug_check_plan(const erc_graph_desc* desc) {
   return guarded([&]() -> erc_status {
     g_last_error.clear();
@@ -1345,6 +1447,7 @@ erc_status erc_debug_check_plan(const erc_graph_desc* desc) {
         if (mh >= nm || P.task_chunk[t] < 0 || P.task_chunk[t] >= P.mega_nchunk[mh])
           return bad("chunk index out of range");
         if (P.mega_chunk0[mh] + P.mega_nchunk[mh] > P.nslot) return bad("chunk slots out of range");
+        if (P.mega_row[mh] != i) return bad("chunk of a split row names another row");
         seen_chunks[mh] += 1;
       } else if (P.task_beg[t] != rp[i] || P.task_end[t] != rp[i + 1]) {
         return bad("single-chunk task does not cover its row");

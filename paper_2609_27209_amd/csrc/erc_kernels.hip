@@ -356,7 +356,6 @@ struct SpmmArgs {
   void* q;
   void* chunkbuf;
   double* mega_dots;  // nmega x 3 x kb pairs
-  uint32_t* mega_tick;
   double* part;       // grid x 3 x kb pairs: this launch's block partials
   const int32_t* gate;
   double delta;
@@ -367,7 +366,9 @@ struct SpmmArgs {
 // q.q accumulated in at least twice the working precision (with the Jacobi variant the
 // last two are weighted by m_i = 1/(d_i + delta): (m r).q and (m q).q).  Block tasks (long rows,
 // split over the 4 waves of a block and, beyond one block's share, over several
-// blocks) run first; then each wave walks its own contiguous range of short rows.
+// blocks) run first; then each wave walks its own contiguous range of short rows.  A row
+// split over several blocks only stores its chunk sums here; k_mega_fin, the next
+// launch on the stream, adds them, so no block needs a device-scope fence.
 template <typename T, int LPN, bool W>
 // At most 128 VGPRs (four waves per SIMD): the 32-column instantiation would take 138
 // and fall to three waves, which costs more than its few spilled registers.
@@ -377,7 +378,6 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   if (*a.gate == 0) return;
   __shared__ DDv s_dots[kWavesPerBlock][3 * KB];
   __shared__ V<T> s_acc[kWavesPerBlock][LPN];
-  __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
@@ -394,9 +394,9 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   // finished by group 0 of wave 0)
   Dot<T> ldots[3 * VEC];
 
-  // finish one row of a block task in group-0 lanes: q = delta p_i + acc, store, and
-  // accumulate the dots (into this lane's partials, or as this row's own pairs at `dst`)
-  auto finish = [&](int i, const V<T>& pi, const V<T>& acc, DDv* dst) {
+  // finish one row in group-0 lanes: q = delta p_i + acc, store, and accumulate the dots
+  // into this lane's partials
+  auto finish = [&](int i, const V<T>& pi, const V<T>& acc) {
     V<T> qv;
     const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
 #pragma unroll
@@ -404,20 +404,11 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
     stv_nt(Q + off, qv);
     const V<T> ri = ldv_nt(Rr + off);
     const T mi = pc ? minv[i] : T(1);
-    if (dst == nullptr) {
 #pragma unroll
-      for (int v = 0; v < VEC; ++v) {
-        ldots[v].add(pi.x[v], qv.x[v]);
-        ldots[VEC + v].add(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
-        ldots[2 * VEC + v].add(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < VEC; ++v) {
-        dst[sub * VEC + v] = Dot<T>::one(pi.x[v], qv.x[v]);
-        dst[KB + sub * VEC + v] = Dot<T>::one(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
-        dst[2 * KB + sub * VEC + v] = Dot<T>::one(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
-      }
+    for (int v = 0; v < VEC; ++v) {
+      ldots[v].add(pi.x[v], qv.x[v]);
+      ldots[VEC + v].add(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
+      ldots[2 * VEC + v].add(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
     }
   };
 
@@ -444,30 +435,13 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
         for (int v = 0; v < VEC; ++v) tot.x[v] += x.x[v];
       }
     }
-    if (mh < 0) {
-      if (wv == 0 && lane < LPN) finish(i, pi, tot, nullptr);
-    } else {
-      T* cb = static_cast<T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
-      if (wv == 0 && lane < LPN) stv(cb + static_cast<int64_t>(a.g.task_chunk[t]) * KB + sub * VEC, tot);
-      __threadfence();
-      __syncthreads();
-      if (threadIdx.x == 0)
-        s_last = (atomicAdd(&a.mega_tick[mh], 1u) ==
-                  static_cast<unsigned>(a.g.mega_nchunk[mh] - 1));
-      __syncthreads();
-      if (s_last) {
-        __threadfence();
-        if (wv == 0 && lane < LPN) {
-          V<T> rs = vzero<T>();
-          const int nch = a.g.mega_nchunk[mh];
-          for (int k = 0; k < nch; ++k) {
-            const V<T> x = ldv(cb + static_cast<int64_t>(k) * KB + sub * VEC);
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) rs.x[v] += x.x[v];
-          }
-          finish(i, pi, rs, reinterpret_cast<DDv*>(a.mega_dots) + static_cast<int64_t>(mh) * 3 * KB);
-        }
-        if (threadIdx.x == 0) a.mega_tick[mh] = 0u;
+    if (wv == 0 && lane < LPN) {
+      if (mh < 0) {
+        finish(i, pi, tot);
+      } else {
+        // one chunk of a split row: its sum goes to the row's chunk slot, k_mega_fin adds
+        T* cb = static_cast<T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
+        stv(cb + static_cast<int64_t>(a.g.task_chunk[t]) * KB + sub * VEC, tot);
       }
     }
     __syncthreads();
@@ -512,7 +486,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
           V<T> accr = vzero<T>();
           gather_row<T, LPN, W>(a.g.col, wgt, P, ir, lr.beg, lr.beg + lr.deg, pir, accr, lane);
           reduce_groups<T, LPN>(accr);
-          if (lane < LPN) finish(ir, pir, accr, nullptr);
+          if (lane < LPN) finish(ir, pir, accr);
         }
         continue;
       }
@@ -599,6 +573,52 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   __syncthreads();
   DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * 3 * KB;
   for (int v = threadIdx.x; v < 3 * KB; v += kBlock) part[v] = s_dots[0][v];
+}
+
+// Rows split over several blocks of the SpMM: one wavefront per row adds the row's
+// chunk sums in chunk order (the order the chunks cover the row), forms q_i =
+// delta p_i + sum, and stores the row's p.q, r.q, q.q terms as its own compensated pairs
+// (nmega x 3 x kb), which k_fin_col adds to the column totals.  Running in the launch
+// after the SpMM makes the chunk sums visible without a device-scope fence.
+template <typename T, int LPN>
+__global__ __launch_bounds__(64) void k_mega_fin(SpmmArgs a) {
+  constexpr int VEC = V<T>::N;
+  constexpr int KB = LPN * VEC;
+  if (*a.gate == 0) return;
+  const int mh = blockIdx.x;
+  const int sub = threadIdx.x;
+  if (sub >= LPN) return;
+  const int i = a.g.mega_row[mh];
+  const int nch = a.g.mega_nchunk[mh];
+  const T* __restrict__ cb =
+      static_cast<const T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
+  V<T> rs = vzero<T>();
+  for (int k = 0; k < nch; ++k) {
+    const V<T> x = ldv(cb + static_cast<int64_t>(k) * KB + sub * VEC);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) rs.x[v] += x.x[v];
+  }
+  const T* __restrict__ P = static_cast<const T*>(a.p);
+  const T* __restrict__ Rr = static_cast<const T*>(a.r);
+  T* __restrict__ Q = static_cast<T*>(a.q);
+  const T* __restrict__ minv = static_cast<const T*>(a.minv);
+  const bool pc = minv != nullptr;
+  const T dlt = static_cast<T>(a.delta);
+  const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
+  const V<T> pi = ldv(P + off);
+  V<T> qv;
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + rs.x[v];
+  stv_nt(Q + off, qv);
+  const V<T> ri = ldv_nt(Rr + off);
+  const T mi = pc ? minv[i] : T(1);
+  DDv* dst = reinterpret_cast<DDv*>(a.mega_dots) + static_cast<int64_t>(mh) * 3 * KB;
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) {
+    dst[sub * VEC + v] = Dot<T>::one(pi.x[v], qv.x[v]);
+    dst[KB + sub * VEC + v] = Dot<T>::one(pc ? ri.x[v] * mi : ri.x[v], qv.x[v]);
+    dst[2 * KB + sub * VEC + v] = Dot<T>::one(pc ? qv.x[v] * mi : qv.x[v], qv.x[v]);
+  }
 }
 
 // Level-1 sum of the block partials written by the previous launch: block b of this
@@ -1350,16 +1370,22 @@ __global__ __launch_bounds__(kBlock) void k_normalise(DevGraph g, const double* 
                                                       double* __restrict__ pe) {
   const double tn = totals[2];
   const double te = totals[3];
+  // a NaN or infinite kappa (flagged by k_minmax) makes every probability NaN, rather
+  // than letting the NaN weight fall back to the uniform distribution
+  const bool bad = totals[4] != 0.0;
+  const double nan = __longlong_as_double(0x7ff8000000000000ll);
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < g.n; i += stride) {
-    if (tn > 0.0) {
+    if (bad) {
+      pn[i] = nan;
+    } else if (tn > 0.0) {
       pn[i] = pn[i] / tn;
     } else {
       pn[i] = (g.rowptr[i + 1] > g.rowptr[i]) ? inv_nonisolated : 0.0;
     }
   }
   for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < g.m; e += stride)
-    pe[e] = pe[e] / te;
+    pe[e] = bad ? nan : pe[e] / te;
 }
 
 // ---------------------------------------------------------------------------------
@@ -1503,6 +1529,11 @@ static hipError_t spmm_launch(const SpmmArgs& a, hipStream_t s) {
     ERC_LAUNCH((k_spmm<T, LPN, true>), a.g.grid, s, a);
   else
     ERC_LAUNCH((k_spmm<T, LPN, false>), a.g.grid, s, a);
+  if (a.g.nmega > 0) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_mega_fin<T, LPN>), dim3(a.g.nmega), dim3(64), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -1515,7 +1546,6 @@ hipError_t launch_spmm(const DevGraph& g, const Work& w, erc_dtype dt, double de
   a.q = q;
   a.chunkbuf = w.chunkbuf;
   a.mega_dots = w.mega_dots;
-  a.mega_tick = w.mega_tick;
   a.part = w.part;
   a.gate = gate;
   a.delta = delta;

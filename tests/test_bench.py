@@ -36,18 +36,39 @@ def test_padded_widths():
 
 @pytest.mark.parametrize("weighted", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "f64"])
-def test_spmm_byte_model_reads_each_array_once(weighted, dtype):
+def test_spmm_byte_models(weighted, dtype):
     g = gen.erdos_renyi(300, 0.03, 7, weighted=weighted)
     kb = 32
     vt = np.float32 if dtype == "f32" else np.float64
-    # the arrays one launch streams: column indices, weights in the working precision,
-    # row pointers, and the n x kb blocks p (read), r (read) and q (written)
-    arrays = [g.col.astype(np.int32), g.rowptr.astype(np.int64)]
+    # compulsory bytes: column indices, weights in the working precision, row pointers,
+    # the diagonal (one n-vector) and the n x kb blocks p (read) and q (written)
+    arrays = [g.col.astype(np.int32), g.rowptr.astype(np.int64), np.zeros(g.n, vt)]
     if weighted:
         arrays.append(np.asarray(g.w).astype(vt))
     block = np.zeros((g.n, kb), dtype=vt)
-    expect = sum(a.nbytes for a in arrays) + 3 * block.nbytes
+    expect = sum(a.nbytes for a in arrays) + 2 * block.nbytes
     assert bench.spmm_bytes_per_launch(g, kb, dtype) == expect
+    # what the fused kernel streams: no diagonal, plus r for the fused r.q
+    assert bench.spmm_fused_bytes_per_launch(g, kb, dtype) == \
+        expect - g.n * vt().itemsize + block.nbytes
+    # an iteration counts 11 n x kb passes in all (SpMM: p, q; a z, r update reading z, p,
+    # r, q and writing z, r; a p update reading r, p and writing p): 9 beyond the SpMM's
+    assert bench.iteration_bytes(g, kb, dtype) == expect + 9 * block.nbytes
+
+
+def test_byte_model_of_the_largest_workload():
+    """4 nnz + 4 nnz + 8 (n+1) + 4 n + 2 * 4 * n * 64 on the 2.4M-node workload's shape
+    (n = 2.4M, nnz = 124M, weighted, fp32, 64 columns) is 2.2496 GB."""
+    class Shape:
+        n = 2_400_000
+        nnz = 124_000_000
+        w = True
+    assert bench.spmm_bytes_per_launch(Shape, 64, "f32") == 2_249_600_008
+
+
+def test_host_cpu_record():
+    c = bench.host_cpu()
+    assert c["nproc"] >= 1 and 1 <= c["usable"] <= max(c["nproc"], c["usable"]) and c["model"]
 
 
 def _gpu():
@@ -82,8 +103,18 @@ def test_bench_line(monkeypatch, capsys):
     assert math.isclose(r["achieved"], r["bytes_per_launch"] / (r["avg_launch_ms"] / 1e3) / 1e9,
                         rel_tol=1e-3 + 0.5e-4 / r["avg_launch_ms"])
     assert r["traffic"] is None  # counters were taken on the 2.4M-node workload only
+    il = r["inner_loop"]
+    assert il["iterations"] == r["launches_full"] and 0.0 < il["frac"] < 1.0
+    gc = r["gather_ceiling"]
+    assert gc["gathered_bytes"] == g.nnz * 64 * 4 and gc["ms"] > 0
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["cores"] >= 1 and c["value"] > 0 and c["sample"]
+    assert c["processes"] == c["cores"] and c["nproc"] >= 1 and c["cpu_model"]
+    cfg = d["config"]
+    assert (cfg["deg_min"], cfg["deg_max"], cfg["components"]) == \
+        (g.summary()["deg_min"], g.summary()["deg_max"], gen.component_count(g))
+    rc = d["relabelled_copy"]
+    assert rc["ms_per_step"] > 0 and rc["iters_max"] > 0
     assert d["subgraph_draw"]["edges"]["draws"] == max(1, g.m // 1000)
 
 

@@ -42,6 +42,35 @@ def test_lg_matches_dense_jl_per_edge(result):
         assert rel_k.max() < 1e-3, (K, rel_k.max())
 
 
+@pytest.mark.parametrize("K", [1024, 4096])
+def test_lg_matches_oracle_cg_per_edge(result, K):
+    """ERC-LG on the GPU against the oracle's own ERC-LG (same sketch, same CG, same
+    tolerance and stopping rule; Algorithm 1) at the fp32 path's 1e-4: R relative per
+    edge, kappa over its Eq. 2 scale 2 (s_u + s_v) / R + |kappa|, s_u = 1/2 sum_v w_uv R_uv."""
+    import gen
+    from oracle import erc as OE
+    from oracle import graph as OG
+
+    meta, gold, rows, lg = result
+    R, kappa, info = lg[K]
+    g = gen.make_graph(meta["workload"])
+    p = gen.CONFIGS[meta["workload"]].params
+    Ro, oinfo = OE.resistance(g, K, p.k_block, p.delta, p.tol, p.max_iter, p.seed, p.dtype)
+    _, ko = OE.curvature(g, Ro)
+    eu, ev, eid = OG.canonical_edges(g)
+    rows_ = OG.entry_rows(g)
+    w = np.ones(g.nnz) if g.w is None else np.asarray(g.w, np.float64)
+    s = 0.5 * np.bincount(rows_, weights=w * Ro[eid], minlength=g.n)
+    rel_R = np.abs(R - Ro) / Ro
+    rel_k = np.abs(kappa - ko) / (2.0 * (s[eu] + s[ev]) / Ro + np.abs(ko))
+    q = np.quantile(rel_R, [0.5, 0.999])
+    print(f"K={K}: R vs oracle CG max {rel_R.max():.2e} p99.9 {q[1]:.2e} median {q[0]:.2e}; "
+          f"kappa (scaled) {rel_k.max():.2e}; GPU iters {info['iters_max']}, oracle "
+          f"{max(int(i.max()) for i in oinfo.iters)}")
+    assert rel_R.max() <= 1e-4, rel_R.max()
+    assert rel_k.max() <= 1e-4, rel_k.max()
+
+
 def test_lg_and_jl_scores_nearly_identical(result):
     meta, gold, rows, lg = result
     by = {(r["K"], r["method"]): r for r in rows}

@@ -96,8 +96,9 @@ MUTANTS = [
      "if np.any(np.diff(key) < 0):"),
     ("base_is_the_seed", "hashing.py", "return U64(splitmix64(seed, 1)[0])", "return U64(seed)"),
     # the column-parallel driver
-    ("parallel_ranges_overlap", "parallel.py", "jobs = [(bounds[k], bounds[k + 1], prm,",
-     "jobs = [(bounds[k], min(bounds[k + 1] + 1, col_end), prm,"),
+    ("parallel_ranges_overlap", "parallel.py",
+     "chunks = [(bounds[k], bounds[k + 1]) for k in range(procs)]",
+     "chunks = [(bounds[k], min(bounds[k + 1] + 1, col_end)) for k in range(procs)]"),
     ("dense_Q_scale", "exact.py", "np.arange(col0, col0 + ncols)) / math.sqrt(K)",
      "np.arange(col0, col0 + ncols)) / K"),
     ("reg_resistance_sign", "exact.py", "return M[eu, eu] + M[ev, ev] - 2.0 * M[eu, ev]",
