@@ -357,7 +357,8 @@ def jacobi_variant(G, g, p, R_plain, torch):
 
 def per_config_table(steps: int, warmup: int):
     """Every workload at its own solve parameters: curvature edges/s and m*K/s end to
-    end (resistance + curvature + sampling probabilities, inputs in HBM), iterations,
+    end (resistance + curvature + sampling probabilities, inputs in HBM), with and
+    without HIP-graph replay of the iteration groups, iterations,
     average SpMM launch, one step of the Jacobi variant (time and iterations; one run,
     after the timed steps), and the device memory the caller allocates (graph buffer,
     workspace, R, p, kappa and both probability vectors, sampling scratch) for block
@@ -375,20 +376,30 @@ def per_config_table(steps: int, warmup: int):
         g = gen.make_graph(name, progress=log)
         G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=p.dtype)
 
-        def step(profile):
+        def step(profile, graph=True):
             R, info = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed,
-                                   profile=profile)
+                                   profile=profile, graph=graph)
             _, kk = G.curvature(R)
             G.sampling_probs(kk, p.eta)
             return info
 
         for _ in range(warmup):
             step(False)
+        # timed steps as a caller runs them (iteration groups replayed as HIP graphs),
+        # the same steps with every launch enqueued separately, then one step with the
+        # SpMM launches timed by events (which enqueues them separately too)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        infos = [step(True) for _ in range(steps)]
+        for _ in range(steps):
+            step(False)
         torch.cuda.synchronize()
         sec = (time.perf_counter() - t0) / steps
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step(False, graph=False)
+        torch.cuda.synchronize()
+        sec_nograph = (time.perf_counter() - t0) / steps
+        infos = [step(True)]
         full = sum(i["spmm_full"] for i in infos)
         avg = sum(i["ms_spmm"] for i in infos) / max(full, 1)
         kb = padded(p.k_block, p.dtype)
@@ -411,6 +422,7 @@ def per_config_table(steps: int, warmup: int):
         mem = {str(b): gbytes + _abi.erc_workspace_bytes(G.handle, b) + outputs for b in widths}
         rows.append({"workload": name, "n": g.n, "m": g.m, "K": p.K, "k_block": p.k_block,
                      "dtype": p.dtype, "ms_per_step": round(sec * 1e3, 2),
+                     "ms_per_step_without_graphs": round(sec_nograph * 1e3, 2),
                      "edges_per_s": g.m / sec, "edge_columns_per_s": g.m * p.K / sec,
                      "iters_max": infos[-1]["iters_max"],
                      "spmm_avg_ms": round(avg, 4),
