@@ -214,6 +214,19 @@ erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta,
                               void* scratch_dev, size_t scratch_bytes,
                               double* node_prob_dev, double* edge_prob_dev, void* stream);
 
+/* erc_sampling_probs without a scratch argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same kernels and outputs as erc_sampling_probs; the scratch is a
+ * fixed device array of the library (64 KiB per GPU, held until the process ends;
+ * every graph's sampling scratch fits, ERC_E_WORKSPACE otherwise).  Every call on one
+ * GPU uses that GPU's array, so calls that overlap on one GPU race: order them on one
+ * stream.  The handle's device must be current.  Asynchronous: nothing is allocated
+ * and the call does not wait, so a NaN or infinite kappa_e is not reported by status;
+ * every probability is then written as NaN. */
+erc_status erc_sampling_probs_static(erc_handle h, const double* kappa_dev, double eta,
+                                     double* node_prob_dev, double* edge_prob_dev,
+                                     void* stream);
+
 /* ---- curvature-guided subgraph draws (Section 3.2; Section 4) --------------------- */
 
 /* Which distribution a draw uses and what a subgraph is built from. */

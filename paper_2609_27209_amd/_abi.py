@@ -93,6 +93,7 @@ _SIGNATURES = {
     "erc_sampling_scratch_bytes": [c_void_p, POINTER(c_size_t)],
     "erc_sampling_probs": [c_void_p, c_void_p, c_double, c_void_p, c_size_t, c_void_p, c_void_p,
                            c_void_p],
+    "erc_sampling_probs_static": [c_void_p, c_void_p, c_double, c_void_p, c_void_p, c_void_p],
     "erc_draw_scratch_bytes": [c_void_p, c_int, POINTER(c_size_t)],
     "erc_draw": [c_void_p, c_int, c_void_p, c_int64, c_uint64, c_void_p, c_size_t, c_void_p,
                  c_void_p],
@@ -218,6 +219,12 @@ def erc_sampling_probs(h: int, kappa_dev: int, eta: float, scratch: int, scratch
     _check(load().erc_sampling_probs(c_void_p(h), c_void_p(kappa_dev), eta, c_void_p(scratch),
                                      scratch_bytes, c_void_p(pn_dev), c_void_p(pe_dev),
                                      c_void_p(stream)))
+
+
+def erc_sampling_probs_static(h: int, kappa_dev: int, eta: float, pn_dev: int, pe_dev: int,
+                              stream: int) -> None:
+    _check(load().erc_sampling_probs_static(c_void_p(h), c_void_p(kappa_dev), eta,
+                                            c_void_p(pn_dev), c_void_p(pe_dev), c_void_p(stream)))
 
 
 def erc_probe_out_bytes(count: int, row_bytes: int) -> int:

@@ -2,7 +2,8 @@
 
     python -m paper_2609_27209_amd.build
 
-Compiles ``csrc/erc_kernels.hip``, ``csrc/erc_draw.hip``, ``csrc/erc_probe.hip`` and ``csrc/erc_host.cpp`` with
+Compiles ``csrc/erc_kernels.hip``, ``csrc/erc_draw.hip``, ``csrc/erc_probe.hip``,
+``csrc/erc_static.hip`` and ``csrc/erc_host.cpp`` with
 hipcc and links them into ``paper_2609_27209_amd/liberc.so``.  Packed fp32 instructions are disabled in
 device code (``-packed-fp32-ops``); the host pass warns that it does not know the
 feature, which is harmless.
@@ -49,7 +50,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(objdir, exist_ok=True)
     objs = []
     jobs = []
-    for name in ("erc_kernels", "erc_draw", "erc_probe"):
+    for name in ("erc_kernels", "erc_draw", "erc_probe", "erc_static"):
         objs.append(os.path.join(objdir, name + ".o"))
         jobs.append([hipcc, f"--offload-arch={ARCH}", *COMMON, *DEVICE, "-c",
                      os.path.join(CSRC, name + ".hip"), "-o", objs[-1]])

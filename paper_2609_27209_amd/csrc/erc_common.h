@@ -148,6 +148,14 @@ struct SampleWork {
 hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,
                            const SampleWork& sw, double* pn, double* pe, hipStream_t s);
 
+// Fixed device scratch (erc_static.hip) of erc_sampling_probs_static.
+constexpr size_t kStaticScratchBytes = 64 << 10;
+// Looks up this process's copy of the array on `device`, which must be current; once
+// per device, later calls return at once.
+hipError_t static_scratch_setup(int device);
+// The looked-up device address, or nullptr before static_scratch_setup succeeded.
+void* static_scratch_ptr(int device);
+
 // Gather probe (erc_probe.hip): rows of sums it stores for `count` indices, and launch.
 int64_t probe_out_rows(int64_t count);
 hipError_t launch_probe_gather(const int32_t* idx, int64_t count, const void* table, int64_t rows,

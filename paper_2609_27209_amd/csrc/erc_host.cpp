@@ -924,6 +924,9 @@ erc_status erc_create(const erc_graph_desc* desc, void* dev_mem, size_t bytes, v
       return cleanup(fail(ERC_E_DEVICE, "hipHostMalloc failed"));
     for (auto& ev : h->ev)
       if (hipEventCreate(&ev) != hipSuccess) return cleanup(fail(ERC_E_DEVICE, "hipEventCreate failed"));
+    // the fixed scratch of erc_sampling_probs_static on this device (that call retries
+    // the lookup if it fails here, so a failure does not stop the handle)
+    (void)static_scratch_setup(h->device);
     // default priority (no priority argument): the stream only records graph captures
     if (hipStreamCreateWithFlags(&h->cap, hipStreamNonBlocking) != hipSuccess)
       return cleanup(fail(ERC_E_DEVICE, "hipStreamCreateWithFlags failed"));
@@ -1195,38 +1198,74 @@ erc_status erc_sampling_scratch_bytes(erc_handle h, size_t* bytes) {
   });
 }
 
+namespace {
+// Enqueue the sampling-probability kernels with their scratch at scratch_dev; with
+// `wait`, bring the non-finite-curvature flag back and report it.
+erc_status sampling_probs_into(erc_graph_s* h, const double* kappa_dev, double eta,
+                               void* scratch_dev, size_t scratch_bytes, double* node_prob_dev,
+                               double* edge_prob_dev, hipStream_t s, bool wait) {
+  if (!(eta > 0.0) || !std::isfinite(eta)) return fail(ERC_E_INVALID_ARG, "eta must be finite and > 0");
+  if (node_prob_dev == nullptr || scratch_dev == nullptr ||
+      (h->m > 0 && (kappa_dev == nullptr || edge_prob_dev == nullptr)))
+    return fail(ERC_E_INVALID_ARG, "NULL buffer");
+  const SampleLayout L = sample_layout(h);
+  if (static_cast<int64_t>(scratch_bytes) < L.total)
+    return fail(ERC_E_WORKSPACE, "scratch smaller than erc_sampling_scratch_bytes (" +
+                                     std::to_string(L.total) + " bytes)");
+  char* b = static_cast<char*>(scratch_dev);
+  SampleWork sw{};
+  sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
+  sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
+  sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
+  sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
+  sw.totals = reinterpret_cast<double*>(b + L.totals);
+  sw.grid = L.grid;
+  // tickets and totals start at zero (fill kernels: a captured stream records no memset)
+  ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
+  ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
+  ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
+  if (!wait) return ERC_OK;
+  // the minimum/maximum pass flags a NaN or infinite kappa (the probabilities are then
+  // written as NaN); the flag comes back to the host so the call can report it
+  double* flag = reinterpret_cast<double*>(h->pinned + kPinSampleFlag);
+  ERC_HIP(hipMemcpyAsync(flag, sw.totals + 4, sizeof(double), hipMemcpyDeviceToHost, s));
+  ERC_HIP(hipStreamSynchronize(s));
+  if (*flag != 0.0) return fail(ERC_E_NUMERIC, "curvature contains NaN or infinite values");
+  return ERC_OK;
+}
+}  // namespace
+
 erc_status erc_sampling_probs(erc_handle h, const double* kappa_dev, double eta, void* scratch_dev,
                               size_t scratch_bytes, double* node_prob_dev, double* edge_prob_dev,
                               void* stream) {
   return guarded([&]() -> erc_status {
     g_last_error.clear();
     if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
-    if (!(eta > 0.0) || !std::isfinite(eta)) return fail(ERC_E_INVALID_ARG, "eta must be finite and > 0");
-    if (node_prob_dev == nullptr || scratch_dev == nullptr ||
-        (h->m > 0 && (kappa_dev == nullptr || edge_prob_dev == nullptr)))
-      return fail(ERC_E_INVALID_ARG, "NULL buffer");
-    const SampleLayout L = sample_layout(h);
-    if (static_cast<int64_t>(scratch_bytes) < L.total)
-      return fail(ERC_E_WORKSPACE, "scratch smaller than erc_sampling_scratch_bytes");
-    char* b = static_cast<char*>(scratch_dev);
-    SampleWork sw{};
-    sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
-    sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
-    sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
-    sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
-    sw.totals = reinterpret_cast<double*>(b + L.totals);
-    sw.grid = L.grid;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
-    ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
-    ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
-    // the minimum/maximum pass flags a NaN or infinite kappa (the probabilities are then
-    // written as NaN); the flag comes back to the host so the call can report it
-    double* flag = reinterpret_cast<double*>(h->pinned + kPinSampleFlag);
-    ERC_HIP(hipMemcpyAsync(flag, sw.totals + 4, sizeof(double), hipMemcpyDeviceToHost, s));
-    ERC_HIP(hipStreamSynchronize(s));
-    if (*flag != 0.0) return fail(ERC_E_NUMERIC, "curvature contains NaN or infinite values");
-    return ERC_OK;
+    return sampling_probs_into(h, kappa_dev, eta, scratch_dev, scratch_bytes, node_prob_dev,
+                               edge_prob_dev, static_cast<hipStream_t>(stream), true);
+  });
+}
+
+erc_status erc_sampling_probs_static(erc_handle h, const double* kappa_dev, double eta,
+                                     double* node_prob_dev, double* edge_prob_dev, void* stream) {
+  return guarded([&]() -> erc_status {
+    g_last_error.clear();
+    if (check_handle(h) != ERC_OK) return ERC_E_INVALID_ARG;
+    int cur = -1;
+    ERC_HIP(hipGetDevice(&cur));
+    if (cur != h->device)
+      return fail(ERC_E_INVALID_ARG, "the handle's device (" + std::to_string(h->device) +
+                                         ") is not the current device (" + std::to_string(cur) + ")");
+    const int64_t need = sample_layout(h).total;
+    if (need > static_cast<int64_t>(kStaticScratchBytes))
+      return fail(ERC_E_WORKSPACE, "needs " + std::to_string(need) + " bytes of scratch; the static "
+                                   "scratch holds " + std::to_string(kStaticScratchBytes));
+    // looked up at erc_create; again here if that lookup failed
+    ERC_HIP(static_scratch_setup(h->device));
+    void* scratch = static_scratch_ptr(h->device);
+    if (scratch == nullptr) return fail(ERC_E_DEVICE, "static scratch address unavailable");
+    return sampling_probs_into(h, kappa_dev, eta, scratch, kStaticScratchBytes, node_prob_dev,
+                               edge_prob_dev, static_cast<hipStream_t>(stream), false);
   });
 }
 
