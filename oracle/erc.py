@@ -35,15 +35,17 @@ def working_dtype(dtype: str):
     return {"f64": np.float64, "f32": np.float32}[dtype]
 
 
-def rhs(g, K: int, col0: int, ncols: int, seed: int, dtype: str = "f64", rows=None):
+def rhs(g, K: int, col0: int, ncols: int, seed: int, dtype: str = "f64", rows=None,
+        edges=None):
     """Y[i, c] = (1/sqrt(K)) * sum_{j in N(i)} B_{e(i,j), i} sqrt(w_e) sign(e, col0 + c).
 
     B_{e,i} is +1 when i is the smaller endpoint of e and -1 otherwise.  The sum over
     j runs in ascending neighbour order in fp64, then the product with 1/sqrt(K) is
     rounded once to the working precision.  ``rows`` restricts the output to a
-    subset of nodes (in the given order).
+    subset of nodes (in the given order); ``edges`` is ``canonical_edges(g)`` when the
+    caller already holds it.
     """
-    eu, ev, eid = GR.canonical_edges(g)
+    eu, ev, eid = GR.canonical_edges(g) if edges is None else edges
     sw = np.sqrt(GR.edge_weights(g))
     rp = np.asarray(g.rowptr)
     col = np.asarray(g.col, dtype=np.int64)
@@ -202,23 +204,27 @@ class ResistanceInfo:
 
 def resistance(g, K: int, k_block: int, delta: float, tol: float, max_iter: int, seed: int,
                dtype: str = "f64", col_begin: int = 0, col_end=None, L=None,
-               precond: str = "none"):
+               precond: str = "none", edges=None):
     """R_hat over columns [col_begin, col_end) of the K-column sketch (Algorithm 1).
 
     Columns are processed in batches of at most ``k_block``; each batch forms Y,
     runs CG (or, with precond="jacobi", the Jacobi-preconditioned variant) and adds
-    its squared edge distances to R before the next batch starts.
+    its squared edge distances to R before the next batch starts.  A caller that
+    passes the Laplacian ``L`` (and optionally ``canonical_edges(g)`` as ``edges``)
+    has validated the graph already; otherwise it is validated here.
     """
     solve = {"none": cg_columns, "jacobi": pcg_columns}[precond]
     col_end = K if col_end is None else col_end
-    GR.check_graph(g)
-    L = GR.laplacian(g) if L is None else L
-    eu, ev, _ = GR.canonical_edges(g)
+    if L is None:
+        GR.check_graph(g)
+        L = GR.laplacian(g)
+    edges = GR.canonical_edges(g) if edges is None else edges
+    eu, ev, _ = edges
     R = np.zeros(eu.size)
     info = ResistanceInfo()
     for c0 in range(col_begin, col_end, k_block):
         nc = min(k_block, col_end - c0)
-        Y = rhs(g, K, c0, nc, seed, dtype)
+        Y = rhs(g, K, c0, nc, seed, dtype, edges=edges)
         res = solve(L, delta, Y, tol, max_iter)
         R += edge_distances(res.Z, eu, ev)
         info.iters.append(res.iters)

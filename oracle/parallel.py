@@ -20,6 +20,7 @@ from . import graph as GR
 
 _G = None
 _L = None
+_E = None
 
 
 def _work(args):
@@ -27,7 +28,7 @@ def _work(args):
     t0 = time.time()
     R, info = erc.resistance(_G, prm["K"], prm["k_block"], prm["delta"], prm["tol"],
                              prm["max_iter"], prm["seed"], prm["dtype"], c0, c1, L=_L,
-                             precond=prm["precond"])
+                             precond=prm["precond"], edges=_E)
     iters = np.concatenate(info.iters) if info.iters else np.zeros(0, np.int64)
     conv = np.concatenate(info.converged) if info.converged else np.zeros(0, bool)
     np.savez(path, R=R, iters=iters, conv=conv, seconds=time.time() - t0)
@@ -42,13 +43,16 @@ def solve_chunks(g, chunks, paths, K, k_block, delta, tol, max_iter, seed, dtype
     Chunks are independent and may come from several disjoint ranges; each file holds
     exactly what ``erc.resistance`` returns for that range alone.
     """
-    global _G, _L
+    global _G, _L, _E
     assert len(chunks) == len(paths)
     if not chunks:
         return
     GR.check_graph(g)
     _G = g
     _L = GR.laplacian(g)
+    # built once here and shared with the forked workers, which then hold only their
+    # columns' vectors
+    _E = GR.canonical_edges(g)
     prm = dict(K=K, k_block=k_block, delta=delta, tol=tol, max_iter=max_iter, seed=seed,
                dtype=dtype, precond=precond)
     jobs = [(c0, c1, prm, path) for (c0, c1), path in zip(chunks, paths)]
@@ -62,6 +66,7 @@ def solve_chunks(g, chunks, paths, K, k_block, delta, tol, max_iter, seed, dtype
     finally:
         _G = None
         _L = None
+        _E = None
 
 
 def resistance_parallel(g, K, k_block, delta, tol, max_iter, seed, dtype="f64", col_begin=0,

@@ -141,16 +141,18 @@ def hub_samples(g, rng):
     return hubs, edges
 
 
-def solve_ranges(g, name, tag, ranges, precond, procs):
-    """R, iterations and flags per range, from cached or newly solved chunks."""
+def solve_ranges(g, name, tag, ranges, precond, procs, tol=None):
+    """R, iterations and flags per range, from cached or newly solved chunks (at the
+    workload's tolerance, or at `tol`; the tag must then name that tolerance)."""
     p = gen.CONFIGS[name].params
+    tol = p.tol if tol is None else tol
     plans = [plan_chunks(tag, c0, c1) for c0, c1 in ranges]
     todo = sorted({c for chunks, new in plans for c, fresh in zip(chunks, new) if fresh})
     if todo:
         log(f"{name}: solving chunks {todo} on {procs} processes")
         t0 = time.time()
         solve_chunks(g, todo, [chunk_path(tag, a, b) for a, b in todo], p.K, p.k_block,
-                     p.delta, p.tol, p.max_iter, p.seed, p.dtype, procs=procs,
+                     p.delta, tol, p.max_iter, p.seed, p.dtype, procs=procs,
                      progress=log, precond=precond)
         log(f"{name}: chunks solved in {time.time() - t0:.0f}s")
     out = []

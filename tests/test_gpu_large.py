@@ -4,9 +4,11 @@ tests/golden/<name>.npz is written by tests/golden/make_golden.py, which runs on
 CPU oracle on the same seeded graph and projection (<name>_jacobi.npz: the oracle's
 Jacobi-preconditioned CG, compared with the GPU's ERC_JACOBI variant).  The GPU runs
 the same column range in the launch configuration of bench.py (same K, block width,
-shift, tolerance and seed; the 2.4M-node workload's stored range is its first 16
-columns, solved in one 64-column block) and is compared at the stored samples of edges
-and nodes:
+shift, tolerance and seed; the 2.4M-node workload's stored ranges are its first
+64-column block and columns 240-255 of its last block, the Jacobi variant's its first
+16 columns) and is compared at the stored samples of edges and nodes (seeded random
+ones, the two extreme-curvature edges, and the 256 highest-degree rows with up to 128
+edges each, which take the long-row work paths of the SpMM):
 
 * R: relative error <= 1e-4;
 * p: error over s_u = 1/2 sum_v w_uv R_uv <= 1e-4;
@@ -45,7 +47,7 @@ def _load(name):
 
 
 @pytest.mark.parametrize("tag", ["cl170k", "cl230k", "cl2400k", "cl2400k_jacobi"])
-def test_stored_oracle_parity(tag):
+def test_stored_oracle_parity(tag, parity_log):
     E = _gpu()
     meta, gold = _load(tag)
     name = meta["workload"]
@@ -71,6 +73,8 @@ def test_stored_oracle_parity(tag):
     pp = pp.cpu().numpy()[ns]
     pn = pn.cpu().numpy()[ns]
     rtol = meta["rtol"]
+    parity_log(tag, R=(R, gold["R"]), p=(pp, gold["p"]), kappa=(kk, gold["kappa"]),
+               node_prob=(pn, gold["node_prob"]), edge_prob=(pe, gold["edge_prob"]))
     rel_R = np.max(np.abs(R - gold["R"]) / gold["R"])
     s = gold["s_node"]
     iso = s == 0

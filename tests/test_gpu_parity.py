@@ -144,7 +144,7 @@ def _run_gpu(E, g, p):
 
 
 @pytest.mark.parametrize("name,rtol", [("er2k", 1e-9), ("sbm20k", 1e-4)])
-def test_pipeline_parity(name, rtol):
+def test_pipeline_parity(name, rtol, parity_log):
     E = _gpu()
     wl = gen.CONFIGS[name]
     g = gen.make_graph(name)
@@ -152,6 +152,8 @@ def test_pipeline_parity(name, rtol):
     ref = OE.run(g, p)
     G, R, pp, kk, pn, pe, info = _run_gpu(E, g, p)
     assert info["cols_unconverged"] == 0 and info["breakdowns"] == 0
+    parity_log(name, R=(R, ref.R), p=(pp, ref.p), kappa=(kk, ref.kappa),
+               node_prob=(pn, ref.node_prob), edge_prob=(pe, ref.edge_prob))
     rel_R, err_p, err_k = _scaled_errors(g, ref.R, ref.p, ref.kappa, R, pp, kk)
     print(f"{name}: R {rel_R:.3e} p {err_p:.3e} kappa {err_k:.3e} iters {info['iters_max']}")
     assert rel_R <= rtol
