@@ -515,6 +515,53 @@ def gather_footprints(name: str, torch):
             "indices": int(col.size), "kernel": "k_probe_gather", "rows": res}
 
 
+def gather_slices(name: str, torch, reps: int = 5):
+    """The gather probe on the workload's own column indices with each p row split into
+    S column slices gathered by separate blocks (block b takes slice b % S, so each XCD's
+    L2 holds one slice of the rows: erc_probe_gather_sliced), for every S that keeps a
+    slice at 64 bytes or more.  Median of `reps` launches after a warm-up, HIP events;
+    the rate counts the whole row (all slices) per index."""
+    import numpy as np
+
+    import gen
+    from paper_2609_27209_amd import _abi
+
+    p = gen.CONFIGS[name].params
+    g = gen.make_graph(name, progress=log)
+    kb = padded(p.k_block, p.dtype)
+    full = kb * elem_bytes(p.dtype)
+    idx = torch.from_numpy(np.ascontiguousarray(g.col, np.int32)).cuda()
+    table = torch.empty(g.n * full // 4, dtype=torch.float32, device="cuda")
+    table.uniform_()
+    st = torch.cuda.current_stream()
+    rows = {}
+    S = 1
+    while full // S >= 64 and S <= 8:
+        rb = full // S
+        out = torch.empty(S * _abi.erc_probe_out_bytes(idx.numel(), rb) // 4,
+                          dtype=torch.float32, device="cuda")
+        ts = []
+        for r in range(reps + 1):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            _abi.erc_probe_gather_sliced(idx.data_ptr(), idx.numel(), table.data_ptr(), g.n, rb,
+                                         S, out.data_ptr(), st.cuda_stream)
+            e1.record(st)
+            torch.cuda.synchronize()
+            if r > 0:
+                ts.append(e0.elapsed_time(e1))
+        ms = sorted(ts)[len(ts) // 2]
+        rows[str(S)] = {"slice_bytes": rb, "ms": round(ms, 4),
+                        "gathered_gbs": round(idx.numel() * full / (ms / 1e3) / 1e9, 1),
+                        "per_xcd_footprint_bytes": g.n * rb}
+        log(f"sliced gather {name} S={S}: {rows[str(S)]}")
+        del out
+        S *= 2
+    return {"table": "gather_slices", "workload": name, "row_bytes": full,
+            "indices": int(idx.numel()), "kernel": "k_probe_gather", "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -543,6 +590,10 @@ def main() -> int:
                     help="instead of the benchmark line: one line with the gather probe's "
                          "rate on the --config workload's column indices and on index "
                          "streams with controlled footprints")
+    ap.add_argument("--gather-slices", action="store_true",
+                    help="instead of the benchmark line: one line with the gather probe's "
+                         "rate on the --config workload's column indices with each row "
+                         "gathered in 1, 2, 4 or 8 column slices by separate blocks")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this size 3 times (a plain "
                          "copy kernel of known size, to calibrate HBM byte counters)")
@@ -572,6 +623,9 @@ def main() -> int:
         return 0
     if args.gather_ceiling:
         print(json.dumps(gather_footprints(args.config, torch)), flush=True)
+        return 0
+    if args.gather_slices:
+        print(json.dumps(gather_slices(args.config, torch)), flush=True)
         return 0
     wl = gen.CONFIGS[args.config]
     p = wl.params

@@ -286,6 +286,18 @@ erc_status erc_probe_out_bytes(int64_t count, int32_t row_bytes, size_t* bytes);
 erc_status erc_probe_gather(const int32_t* idx_dev, int64_t count, const void* table_dev,
                             int64_t rows, int32_t row_bytes, void* out_dev, void* stream);
 
+/* erc_probe_gather over `slices` column slices of each row at once: table_dev holds rows
+ * of slices * row_bytes bytes, and block b of the launch (slices times as many blocks)
+ * gathers the row_bytes at offset (b % slices) * row_bytes of every indexed row for the
+ * index range of b / slices.  Blocks go to the GPU's eight XCDs round-robin, so with
+ * slices dividing 8 each XCD's L2 sees one slice only: this measures what a
+ * column-sliced gather would gain from the smaller per-XCD footprint.  out_dev holds
+ * slices * erc_probe_out_bytes(count, row_bytes) bytes.  slices in 1..64;
+ * erc_probe_gather is slices = 1.  Asynchronous. */
+erc_status erc_probe_gather_sliced(const int32_t* idx_dev, int64_t count, const void* table_dev,
+                                   int64_t rows, int32_t row_bytes, int32_t slices,
+                                   void* out_dev, void* stream);
+
 /* ---- test hooks (same conventions; used by the parity tests) ---------------------- */
 
 /* Host-only self-check of the work plan erc_create would build for this graph (no GPU

@@ -102,6 +102,8 @@ _SIGNATURES = {
                      c_void_p, c_void_p, POINTER(c_int64), c_void_p],
     "erc_probe_out_bytes": [c_int64, c_int32, POINTER(c_size_t)],
     "erc_probe_gather": [c_void_p, c_int64, c_void_p, c_int64, c_int32, c_void_p, c_void_p],
+    "erc_probe_gather_sliced": [c_void_p, c_int64, c_void_p, c_int64, c_int32, c_int32, c_void_p,
+                                c_void_p],
     "erc_status_string": [c_int],
     "erc_last_error": [],
     "erc_debug_check_plan": [POINTER(erc_graph_desc)],
@@ -237,6 +239,13 @@ def erc_probe_gather(idx_dev: int, count: int, table_dev: int, rows: int, row_by
                      out_dev: int, stream: int) -> None:
     _check(load().erc_probe_gather(c_void_p(idx_dev), count, c_void_p(table_dev), rows, row_bytes,
                                    c_void_p(out_dev), c_void_p(stream)))
+
+
+def erc_probe_gather_sliced(idx_dev: int, count: int, table_dev: int, rows: int, row_bytes: int,
+                            slices: int, out_dev: int, stream: int) -> None:
+    _check(load().erc_probe_gather_sliced(c_void_p(idx_dev), count, c_void_p(table_dev), rows,
+                                          row_bytes, slices, c_void_p(out_dev),
+                                          c_void_p(stream)))
 
 
 def erc_draw_scratch_bytes(h: int, items: int) -> int:

@@ -159,7 +159,7 @@ void* static_scratch_ptr(int device);
 // Gather probe (erc_probe.hip): rows of sums it stores for `count` indices, and launch.
 int64_t probe_out_rows(int64_t count);
 hipError_t launch_probe_gather(const int32_t* idx, int64_t count, const void* table, int64_t rows,
-                               int row_bytes, void* out, hipStream_t s);
+                               int row_bytes, int slices, void* out, hipStream_t s);
 
 // Tree sizing helpers (host).
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

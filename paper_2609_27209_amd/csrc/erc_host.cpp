@@ -1422,21 +1422,31 @@ erc_status erc_probe_out_bytes(int64_t count, int32_t row_bytes, size_t* bytes) 
   });
 }
 
-erc_status erc_probe_gather(const int32_t* idx_dev, int64_t count, const void* table_dev,
-                            int64_t rows, int32_t row_bytes, void* out_dev, void* stream) {
+erc_status erc_probe_gather_sliced(const int32_t* idx_dev, int64_t count, const void* table_dev,
+                                   int64_t rows, int32_t row_bytes, int32_t slices,
+                                   void* out_dev, void* stream) {
   return guarded([&]() -> erc_status {
     g_last_error.clear();
     if (count < 0 || rows < 1) return fail(ERC_E_INVALID_ARG, "count must be >= 0 and rows >= 1");
     if (row_bytes < 64 || row_bytes > 1024 || (row_bytes & (row_bytes - 1)) != 0)
       return fail(ERC_E_INVALID_ARG, "row_bytes must be a power of two in 64..1024");
+    if (slices < 1 || slices > 64)
+      return fail(ERC_E_INVALID_ARG, "slices must be in 1..64");
     if (count > 0 && (idx_dev == nullptr || table_dev == nullptr || out_dev == nullptr))
       return fail(ERC_E_INVALID_ARG, "NULL buffer");
     if (reinterpret_cast<uintptr_t>(table_dev) % 16 != 0 || reinterpret_cast<uintptr_t>(out_dev) % 16 != 0)
       return fail(ERC_E_INVALID_ARG, "table and output must be 16-byte aligned");
-    ERC_HIP(launch_probe_gather(idx_dev, count, table_dev, rows, row_bytes, out_dev,
+    if (probe_out_rows(count) * slices > (int64_t{1} << 31) / kWavesPerBlock)
+      return fail(ERC_E_INVALID_ARG, "count * slices too large for one launch");
+    ERC_HIP(launch_probe_gather(idx_dev, count, table_dev, rows, row_bytes, slices, out_dev,
                                 static_cast<hipStream_t>(stream)));
     return ERC_OK;
   });
+}
+
+erc_status erc_probe_gather(const int32_t* idx_dev, int64_t count, const void* table_dev,
+                            int64_t rows, int32_t row_bytes, void* out_dev, void* stream) {
+  return erc_probe_gather_sliced(idx_dev, count, table_dev, rows, row_bytes, 1, out_dev, stream);
 }
 
 erc_status erc_debug_check_plan(const erc_graph_desc* desc) {

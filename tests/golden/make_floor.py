@@ -34,7 +34,7 @@ from oracle import graph as OG  # noqa: E402
 
 TIGHT = 1e-11
 # leading column range solved on the workloads whose whole projection is too long
-COLUMNS = {"cl170k": 16, "cl230k": 8, "cl2400k": 8}
+COLUMNS = {"cl170k": 16, "cl230k": 8, "cl2400k": 4}
 OUT = os.path.join(HERE, "truncation_floor.json")
 
 

@@ -53,7 +53,9 @@ from oracle.parallel import solve_chunks  # noqa: E402
 RANGES = {"cl2400k": [(0, 64), (240, 256)]}
 # the Jacobi-preconditioned variant keeps its stored range
 RANGES_JACOBI = {"cl2400k": [(0, 16)]}
-CHUNK = 8
+# columns per oracle process (ERC_ORACLE_CHUNK overrides: 11 puts the 2.4M-node graph's
+# 80 stored columns on eight processes at once)
+CHUNK = int(os.environ.get("ERC_ORACLE_CHUNK", "8"))
 SAMPLES = 8192
 NHUB = 256
 HUB_EDGES = 128
