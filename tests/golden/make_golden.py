@@ -1,6 +1,6 @@
 """Write the stored oracle values used by the large-workload parity tests.
 
-    python tests/golden/make_golden.py cl170k [cl230k cl2400k cl2400k:jacobi ...]
+    python tests/golden/make_golden.py cl170k [cl230k cl2400k cl2400k:jacobi cl170k:relabel ...]
 
 Each run regenerates the seeded graph, runs the CPU oracle (column-parallel, see
 oracle/parallel.py) over the workload's full projection, or over each column range
@@ -8,7 +8,9 @@ named in RANGES, then computes curvature and sampling probabilities from that R 
 stores the values at seeded samples of edges and nodes in tests/golden/<name>.npz
 (the first range) and tests/golden/<name>_c<begin>.npz (each further range).
 A name with the suffix ":jacobi" solves with the oracle's Jacobi-preconditioned CG
-instead and writes tests/golden/<name>_jacobi.npz.
+instead and writes tests/golden/<name>_jacobi.npz; the suffix ":relabel" solves on a
+copy of the graph with node ids randomly permuted (RELABEL_SEED) and writes
+tests/golden/<name>_relabel.npz.
 Only gen/ and oracle/ are used; nothing here touches the GPU library.  The oracle
 solves columns in chunks of at most CHUNK columns, one process each, and caches every
 chunk's R under $TMPDIR; a range's R is the sum of its chunks in column order, so
@@ -53,6 +55,10 @@ from oracle.parallel import solve_chunks  # noqa: E402
 RANGES = {"cl2400k": [(0, 64), (240, 256)]}
 # the Jacobi-preconditioned variant keeps its stored range
 RANGES_JACOBI = {"cl2400k": [(0, 16)]}
+# ":relabel" runs the workload on a copy with node ids permuted by RELABEL_SEED (no
+# hub-first order), over these column ranges
+RANGES_RELABEL = {"cl170k": [(0, 8)]}
+RELABEL_SEED = 7
 # columns per oracle process (ERC_ORACLE_CHUNK overrides: 11 puts the 2.4M-node graph's
 # 80 stored columns on eight processes at once)
 CHUNK = int(os.environ.get("ERC_ORACLE_CHUNK", "8"))
@@ -172,15 +178,20 @@ def solve_ranges(g, name, tag, ranges, precond, procs, tol=None):
 
 
 def make(spec, procs):
-    name, _, precond = spec.partition(":")
-    precond = precond or "none"
-    tag = name if precond == "none" else f"{name}_{precond}"
+    name, _, variant = spec.partition(":")
+    variant = variant or "none"
+    precond = "jacobi" if variant == "jacobi" else "none"
+    tag = name if variant == "none" else f"{name}_{variant}"
     wl = gen.CONFIGS[name]
     p = wl.params
     t0 = time.time()
     g = gen.make_graph(name, progress=log)
-    log(f"{name}: graph {g.summary()} ({time.time() - t0:.0f}s)")
-    table = RANGES if precond == "none" else RANGES_JACOBI
+    relabel_seed = None
+    if variant == "relabel":
+        relabel_seed = RELABEL_SEED
+        g = gen.relabel(g, np.random.default_rng(RELABEL_SEED).permutation(g.n))
+    log(f"{tag}: graph {g.summary()} ({time.time() - t0:.0f}s)")
+    table = {"none": RANGES, "jacobi": RANGES_JACOBI, "relabel": RANGES_RELABEL}[variant]
     ranges = table.get(name, [(0, p.K)])
     eu, ev, eid = OG.canonical_edges(g)
     rows = OG.entry_rows(g)
@@ -206,6 +217,7 @@ def make(spec, procs):
                 "K": p.K, "k_block": p.k_block, "delta": p.delta, "tol": p.tol,
                 "seed": p.seed, "dtype": p.dtype, "eta": p.eta,
                 "oracle_version": ORACLE_VERSION, "rtol": RTOL, "precond": precond,
+                "relabel_seed": relabel_seed,
                 "chunks": chunks, "solve_process_seconds": round(t_solve, 1),
                 "iters_min": int(iters.min()), "iters_max": int(iters.max()),
                 "iters_total": int(iters.sum()), "converged": bool(conv.all()),

@@ -54,6 +54,9 @@ def test_stored_oracle_parity(tag, parity_log):
     precond = meta.get("precond", "none")
     p = gen.CONFIGS[name].params
     g = gen.make_graph(name)
+    if meta.get("relabel_seed") is not None:
+        # the copy with node ids randomly permuted (no hub-first order)
+        g = gen.relabel(g, np.random.default_rng(meta["relabel_seed"]).permutation(g.n))
     assert g.summary() == meta["graph"], "generator output differs from the stored graph"
     assert (meta["K"], meta["k_block"], meta["seed"]) == (p.K, p.k_block, p.seed)
     G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=p.dtype)
