@@ -355,7 +355,7 @@ def jacobi_variant(G, g, p, R_plain, torch):
     return out
 
 
-def per_config_table(steps: int, warmup: int):
+def per_config_table(steps: int, warmup: int, only=None):
     """Every workload at its own solve parameters: curvature edges/s and m*K/s end to
     end (resistance + curvature + sampling probabilities, inputs in HBM), with and
     without HIP-graph replay of the iteration groups, iterations,
@@ -371,6 +371,8 @@ def per_config_table(steps: int, warmup: int):
 
     rows = []
     for name in gen.configs.ORDER:
+        if only and name not in only:
+            continue
         wl = gen.CONFIGS[name]
         p = wl.params
         g = gen.make_graph(name, progress=log)
@@ -576,6 +578,8 @@ def main() -> int:
     ap.add_argument("--configs", action="store_true",
                     help="instead of the benchmark line: one line with every workload's "
                          "edges/s, iterations, SpMM time and device memory per block width")
+    ap.add_argument("--only", default=None, metavar="NAME,NAME,...",
+                    help="with --configs: only these workloads")
     ap.add_argument("--block-sweep", default=None, metavar="B,B,...",
                     help="instead of the benchmark line: one line with the --config "
                          "workload's step time, iterations and device memory at each of "
@@ -615,7 +619,8 @@ def main() -> int:
         return 1
     torch.cuda.set_device(0)
     if args.configs:
-        print(json.dumps(per_config_table(args.steps, args.warmup)), flush=True)
+        only = set(args.only.split(",")) if args.only else None
+        print(json.dumps(per_config_table(args.steps, args.warmup, only)), flush=True)
         return 0
     if args.block_sweep:
         widths = [int(b) for b in args.block_sweep.split(",")]

@@ -1170,8 +1170,12 @@ struct SampleLayout {
 };
 SampleLayout sample_layout(const erc_graph_s* h) {
   SampleLayout L{};
+  // eight items per thread for the per-edge passes, and at least one block per 32 rows
+  // for the per-node pass (a wavefront per row: on small graphs a grid sized by items
+  // alone left each wavefront a long chain of dependent row loads)
   const int64_t items = std::max(h->n, h->m);
-  L.grid = static_cast<int>(std::min<int64_t>(kSampleGrid, std::max<int64_t>(1, ceil_div(items, kBlock * 8))));
+  const int64_t want = std::max(ceil_div(items, kBlock * 8), ceil_div(h->n, kWavesPerBlock * 8));
+  L.grid = static_cast<int>(std::min<int64_t>(kSampleGrid, std::max<int64_t>(1, want)));
   int64_t off = 0;
   auto take = [&](int64_t bytes) {
     const int64_t at = off;
