@@ -96,6 +96,13 @@ typedef struct {
  * overhead on small graphs; the kernels, their order and the results are the same.
  * ERC_PROFILE_SPMM implies this flag (its events sit between the launches). */
 #define ERC_NO_GRAPH 8u
+/* Enqueue, after every CG update, the exact stopping test that runs only when every
+ * active column is predicted to stop (it saves the one SpMM that would otherwise follow
+ * a block's last update).  By default it is enqueued only where an SpMM gathers at
+ * least 4 GB of neighbour rows (nnz * k_block * element size), because elsewhere the
+ * extra launch per iteration costs more than the SpMM it saves.  Results are the same
+ * either way. */
+#define ERC_EARLY_STOP 16u
 
 /* Parameters of one resistance sweep (Algorithm 1, Require line).
  *  K_total     total projection dimension K; the JL scale is 1/sqrt(K_total) even when
@@ -112,7 +119,8 @@ typedef struct {
  *  check_every iterations enqueued between host convergence polls (0 = default 16);
  *              results do not depend on it
  *  seed        projection seed
- *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH, or 0 */
+ *  flags       ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH |
+ *              ERC_EARLY_STOP, or 0 */
 typedef struct {
   int32_t K_total;
   int32_t k_block;

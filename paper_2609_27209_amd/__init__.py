@@ -120,12 +120,14 @@ class Graph:
 
     @staticmethod
     def params(K, k_block, delta, tol, max_iter=10000, seed=0, col_begin=0, col_end=None,
-               accumulate=False, check_every=0, profile=False, precond="none", graph=True):
+               accumulate=False, check_every=0, profile=False, precond="none", graph=True,
+               early_stop=False):
         if precond not in ("none", "jacobi"):
             raise ValueError(f"precond must be 'none' or 'jacobi', not {precond!r}")
         flags = ((ERC_ACCUMULATE if accumulate else 0) | (ERC_PROFILE_SPMM if profile else 0)
                  | (_abi.ERC_JACOBI if precond == "jacobi" else 0)
-                 | (0 if graph else _abi.ERC_NO_GRAPH))
+                 | (0 if graph else _abi.ERC_NO_GRAPH)
+                 | (_abi.ERC_EARLY_STOP if early_stop else 0))
         return _abi.erc_solve_params(
             K_total=K, k_block=k_block, col_begin=col_begin, col_end=K if col_end is None else col_end,
             delta=delta, tol=tol, max_iter=max_iter, check_every=check_every, seed=seed,
@@ -133,17 +135,18 @@ class Graph:
 
     def resistance(self, K, k_block, delta, tol, max_iter=10000, seed=0, col_begin=0, col_end=None,
                    out=None, accumulate=False, check_every=0, raise_not_converged=True,
-                   profile=False, precond="none", graph=True):
+                   profile=False, precond="none", graph=True, early_stop=False):
         """R (torch fp64, m) over columns [col_begin, col_end) and the solve info dict.
         precond="jacobi" selects the Jacobi-preconditioned CG variant; graph=False
         enqueues every iteration as separate launches instead of replaying a captured
-        group of iterations."""
+        group of iterations; early_stop=True enqueues the early stopping test after
+        every update whatever the graph's size (ERC_EARLY_STOP)."""
         torch = self.torch
         R = out if out is not None else torch.empty(max(self.m, 1), dtype=torch.float64,
                                                     device=self.device)
         ws = self.workspace(k_block)
         prm = self.params(K, k_block, delta, tol, max_iter, seed, col_begin, col_end, accumulate,
-                          check_every, profile, precond, graph)
+                          check_every, profile, precond, graph, early_stop)
         info = _abi.erc_resistance(self.handle, prm, ws.data_ptr(), ws.numel(), R.data_ptr(),
                                    self._stream(), raise_not_converged)
         return R[: self.m], info.as_dict()

@@ -31,6 +31,7 @@ ERC_ACCUMULATE = 1
 ERC_PROFILE_SPMM = 2
 ERC_JACOBI = 4
 ERC_NO_GRAPH = 8
+ERC_EARLY_STOP = 16
 
 
 class erc_graph_desc(ctypes.Structure):

@@ -113,6 +113,7 @@ struct Work {
   double* out;       // small fp64 output area (totals for the host)
   void* minv;        // n: 1 / (d_i + delta) in the working precision (Jacobi variant)
   int pc;            // 1: Jacobi-preconditioned CG, 0: plain CG
+  int fin2;          // 1: enqueue the early exact stopping test after each update
   int32_t grid_rhs, grid_upd, grid_ed;
 };
 

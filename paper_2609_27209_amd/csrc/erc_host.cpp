@@ -75,6 +75,10 @@ constexpr int kMaxGridEd = 8192;
 constexpr int kCountBadGrid = kMaxTreeGrid;
 constexpr int kSampleGrid = 2048;
 constexpr int kDefaultCheck = 16;
+// Neighbour-row bytes one SpMM gathers (nnz * kb * element size) above which each CG
+// iteration also enqueues the early stopping test: 4 GB is about half a millisecond of
+// gathers, against a few microseconds per extra launch and iteration.
+constexpr double kFin2MinGather = 4e9;
 
 size_t dsize(erc_dtype t) { return t == ERC_F32 ? 4 : 8; }
 int64_t align_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
@@ -483,7 +487,7 @@ struct erc_graph_s {
   hipGraphExec_t gexec = nullptr;
   struct GroupKey {
     const void* ws = nullptr;
-    int kb = 0, pc = 0, nb = 0;
+    int kb = 0, pc = 0, nb = 0, fin2 = 0;
     double delta = 0.0;
   } gkey;
 };
@@ -582,6 +586,11 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
   w.out = reinterpret_cast<double*>(b + L.out);
   w.minv = b + L.minv;
   w.pc = pc;
+  // The early stopping test after each update (a third finishing launch, which exits at
+  // once unless every active column is predicted to stop) saves the one SpMM that would
+  // otherwise run after a block's last update, and costs a launch in every iteration.
+  // It pays only where an SpMM is long: gathers of at least kFin2MinGather bytes.
+  w.fin2 = static_cast<double>(h->nnz) * kb * static_cast<double>(dsize(h->dt)) >= kFin2MinGather;
   w.grid_rhs = L.grid_rhs;
   w.grid_upd = L.grid_upd;
   w.grid_ed = L.grid_ed;
@@ -616,7 +625,8 @@ erc_status check_params(const erc_graph_s* h, const erc_solve_params* p) {
   if (!(p->tol > 0.0 && p->tol < 1.0)) return fail(ERC_E_INVALID_ARG, "tol must be in (0, 1)");
   if (p->max_iter < 1) return fail(ERC_E_INVALID_ARG, "max_iter must be >= 1");
   if (p->check_every < 0) return fail(ERC_E_INVALID_ARG, "check_every must be >= 0");
-  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH)) != 0u)
+  if ((p->flags & ~(ERC_ACCUMULATE | ERC_PROFILE_SPMM | ERC_JACOBI | ERC_NO_GRAPH |
+                     ERC_EARLY_STOP)) != 0u)
     return fail(ERC_E_INVALID_ARG, "unknown flag");
   return ERC_OK;
 }
@@ -658,8 +668,8 @@ hipError_t enqueue_iteration(const erc_graph_s* h, const Work& w, double delta, 
   if (e == hipSuccess) e = launch_fin_iter(h->dg, w, 0, s);
   if (e == hipSuccess) e = launch_update(h->dg, w, h->dt, s);
   // the exact stopping test, only when every column is predicted to stop: saves the
-  // SpMM that would otherwise run after the last update
-  if (e == hipSuccess) e = launch_fin_iter(h->dg, w, 2, s);
+  // SpMM that would otherwise run after the last update (on graphs where it pays)
+  if (e == hipSuccess && w.fin2) e = launch_fin_iter(h->dg, w, 2, s);
   return e;
 }
 
@@ -671,10 +681,11 @@ erc_status ensure_group_graph(erc_graph_s* h, const Work& w, double delta, int n
   k.kb = w.kb;
   k.pc = w.pc;
   k.nb = nb;
+  k.fin2 = w.fin2;
   k.delta = delta;
   const erc_graph_s::GroupKey& o = h->gkey;
   if (h->gexec != nullptr && o.ws == k.ws && o.kb == k.kb && o.pc == k.pc && o.nb == k.nb &&
-      o.delta == k.delta)
+      o.fin2 == k.fin2 && o.delta == k.delta)
     return ERC_OK;
   if (h->gexec != nullptr) {
     (void)hipGraphExecDestroy(h->gexec);
@@ -735,7 +746,7 @@ erc_status solve_block(erc_graph_s* h, const erc_solve_params* p, const Work& w,
           ERC_HIP(hipEventRecord(pr[1], s));
           ERC_HIP(launch_fin_iter(h->dg, w, 0, s));
           ERC_HIP(launch_update(h->dg, w, h->dt, s));
-          ERC_HIP(launch_fin_iter(h->dg, w, 2, s));
+          if (w.fin2) ERC_HIP(launch_fin_iter(h->dg, w, 2, s));
         } else {
           ERC_HIP(enqueue_iteration(h, w, p->delta, s));
         }
@@ -1077,7 +1088,8 @@ erc_status erc_resistance(erc_handle h, const erc_solve_params* params, void* ws
     if (static_cast<int64_t>(ws_bytes) < L.total)
       return fail(ERC_E_WORKSPACE, "workspace smaller than erc_workspace_bytes");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    if (params->flags & ERC_EARLY_STOP) w.fin2 = 1;
     st = prepare_work(h, w, L, s);
     if (st != ERC_OK) return st;
     hipEvent_t t0 = h->ev[6], t1 = h->ev[7];
@@ -1603,7 +1615,8 @@ erc_status erc_debug_solve_block(erc_handle h, const erc_solve_params* params, i
     const WorkLayout L = work_layout(h, kb);
     if (static_cast<int64_t>(ws_bytes) < L.total) return fail(ERC_E_WORKSPACE, "workspace too small");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    Work w = carve_work(h, kb, ws_dev, L, (params->flags & ERC_JACOBI) ? 1 : 0);
+    if (params->flags & ERC_EARLY_STOP) w.fin2 = 1;
     st = prepare_work(h, w, L, s);
     if (st != ERC_OK) return st;
     BlockStats bs;

@@ -93,3 +93,25 @@ def test_non_finite_curvature_is_reported(bad):
     ref_pn, ref_pe = OE.sampling_probs(g, kappa.cpu().numpy(), 1e-12)
     np.testing.assert_allclose(pn.cpu().numpy(), ref_pn, rtol=1e-12, atol=0)
     np.testing.assert_allclose(pe.cpu().numpy(), ref_pe, rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+@pytest.mark.parametrize("precond", ["none", "jacobi"])
+def test_early_stop_test_changes_nothing_but_one_spmm(name, precond):
+    """The early exact stopping test after each update (ERC_EARLY_STOP; by default only
+    on graphs whose SpMM gathers several GB) gives the same bits and iteration counts as
+    leaving the test to the next finishing step; it saves at most one SpMM per block,
+    the one that would follow the block's last update.  Both with graph replay and with
+    separate launches."""
+    E = _gpu()
+    make, dtype, K, kb, delta, tol = CASES[name]
+    g = make()
+    G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=dtype)
+    for graph in (True, False):
+        R0, i0 = G.resistance(K, kb, delta, tol, 10000, 17, graph=graph, precond=precond)
+        R0 = R0.cpu().numpy()
+        R1, i1 = G.resistance(K, kb, delta, tol, 10000, 17, graph=graph, precond=precond,
+                              early_stop=True)
+        np.testing.assert_array_equal(R1.cpu().numpy(), R0)
+        assert i1["iters_total"] == i0["iters_total"] and i1["iters_max"] == i0["iters_max"]
+        assert 0 <= i0["spmm_full"] - i1["spmm_full"] <= i0["blocks"]
