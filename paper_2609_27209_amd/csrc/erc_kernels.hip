@@ -678,7 +678,7 @@ struct IterArgs {
 //             count; the last block to finish publishes it.
 // mode 0: both steps; 1: the stopping test only; 2: the stopping test only, and only
 // when the previous mode-0 step predicted that every active column stops.
-constexpr int kFinDirectMax = 1024;  // longest partial set k_fin_col sums by itself
+constexpr int kFinDirectMax = 2048;  // longest partial set k_fin_col sums by itself
 
 template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_sum(IterArgs a) {
@@ -755,7 +755,17 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
     }
     DDv acc = DDv{0.0, 0.0};
     if (need) {
-      for (int t = tid; t < cnt; t += kBlock) {
+      // this thread's elements t = tid, tid + kBlock, ... added in that order; eight
+      // loads are issued before they are added, which leaves the sum unchanged
+      int t = tid;
+      for (; t + 7 * kBlock < cnt; t += 8 * kBlock) {
+        DDv x[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) x[u] = src[static_cast<int64_t>(t + u * kBlock) * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc = (t + u * kBlock == tid) ? x[u] : dd_add(acc, x[u]);
+      }
+      for (; t < cnt; t += kBlock) {
         const DDv x = src[static_cast<int64_t>(t) * stride];
         acc = (t == tid) ? x : dd_add(acc, x);
       }
