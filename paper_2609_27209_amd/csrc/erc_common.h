@@ -142,8 +142,10 @@ hipError_t launch_endpoints(const DevGraph& g, int32_t* u, int32_t* v, hipStream
 hipError_t launch_eids(const DevGraph& g, int32_t* out, hipStream_t s);
 
 struct SampleWork {
-  Tree tree;
-  double* totals;    // [0] -kappa_min, [1] kappa_max, [2] node sum, [3] edge sum, [4] bad count
+  double* part_mm;   // grid x 3 block partials (-kappa_min, kappa_max, non-finite flag),
+                     // then grid edge-weight block sums
+  double* part_n;    // up to grid node-weight block sums
+  double* totals;    // [0] -kappa_min, [1] kappa_max, [2] node sum, [3] edge sum, [4] bad flag
   int32_t grid;
 };
 hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,

@@ -73,7 +73,11 @@ static_assert((kMaxGridUpd + kTreeFan - 1) / kTreeFan <= kMaxTreeGrid,
               "level-1 sums of the update partials must fit the tree buffers");
 constexpr int kMaxGridEd = 8192;
 constexpr int kCountBadGrid = kMaxTreeGrid;
-constexpr int kSampleGrid = 2048;
+// Grid cap of the sampling passes: their scratch is 4 doubles per block plus 64 bytes,
+// 33 KB at the cap, inside the fixed scratch of erc_sampling_probs_static.
+constexpr int kSampleGrid = 1024;
+static_assert(int64_t{kSampleGrid} * 4 * 8 + 3 * 256 <= static_cast<int64_t>(kStaticScratchBytes),
+              "the sampling scratch at the grid cap must fit the fixed scratch");
 constexpr int kDefaultCheck = 16;
 // Neighbour-row bytes one SpMM gathers (nnz * kb * element size) above which each CG
 // iteration also enqueues the early stopping test: 4 GB is about half a millisecond of
@@ -1177,7 +1181,7 @@ erc_status erc_curvature(erc_handle h, const double* R_dev, double* p_dev, doubl
 
 namespace {
 struct SampleLayout {
-  int64_t lvl0, lvl1, lvl2, tick, totals, total;
+  int64_t part_mm, part_n, totals, total;
   int grid;
 };
 SampleLayout sample_layout(const erc_graph_s* h) {
@@ -1194,10 +1198,8 @@ SampleLayout sample_layout(const erc_graph_s* h) {
     off = align_up(off + std::max<int64_t>(bytes, 0), 256);
     return at;
   };
-  L.lvl0 = take(static_cast<int64_t>(L.grid) * 3 * 8);
-  L.lvl1 = take(ceil_div(L.grid, kTreeFan) * 3 * 8);
-  L.lvl2 = take(ceil_div(L.grid, kTreeFan * kTreeFan) * 3 * 8);
-  L.tick = take(tree_ticks(L.grid) * 4);
+  L.part_mm = take(static_cast<int64_t>(L.grid) * 3 * 8);
+  L.part_n = take(static_cast<int64_t>(L.grid) * 8);
   L.totals = take(8 * 8);
   L.total = off;
   return L;
@@ -1230,15 +1232,12 @@ erc_status sampling_probs_into(erc_graph_s* h, const double* kappa_dev, double e
                                      std::to_string(L.total) + " bytes)");
   char* b = static_cast<char*>(scratch_dev);
   SampleWork sw{};
-  sw.tree.lvl0 = reinterpret_cast<double*>(b + L.lvl0);
-  sw.tree.lvl1 = reinterpret_cast<double*>(b + L.lvl1);
-  sw.tree.lvl2 = reinterpret_cast<double*>(b + L.lvl2);
-  sw.tree.tick = reinterpret_cast<uint32_t*>(b + L.tick);
+  sw.part_mm = reinterpret_cast<double*>(b + L.part_mm);
+  sw.part_n = reinterpret_cast<double*>(b + L.part_n);
   sw.totals = reinterpret_cast<double*>(b + L.totals);
   sw.grid = L.grid;
-  // tickets and totals start at zero (fill kernels: a captured stream records no memset)
-  ERC_HIP(launch_fill_u32(sw.tree.tick, 0u, tree_ticks(L.grid), s));
-  ERC_HIP(launch_fill_f64(sw.totals, 0.0, 8, s));
+  // every partial and total is written before it is read, in stream order: nothing is
+  // cleared and no ticket is kept between calls
   ERC_HIP(launch_sampling(h->dg, kappa_dev, eta, h->nonisolated, sw, node_prob_dev, edge_prob_dev, s));
   if (!wait) return ERC_OK;
   // the minimum/maximum pass flags a NaN or infinite kappa (the probabilities are then

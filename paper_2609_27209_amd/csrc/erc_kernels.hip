@@ -1269,12 +1269,47 @@ __global__ __launch_bounds__(kBlock) void k_copy_cols(const T* __restrict__ src,
 }
 
 // ---- sampling (Eqs. 7, 8) --------------------------------------------------------
+// Four launches and no device-scope fence: each launch stores one partial per block and
+// the next launch reduces the previous one's partials itself.  That reduction is done
+// redundantly by every block that needs the total, in the same fixed order in each
+// (thread t adds partials t, t + kBlock, ... in turn, then the block adds the threads'
+// sums in a fixed tree), so every block sees the same bits.
 
-// totals[0] = -kappa_min, totals[1] = kappa_max, totals[4] = 1 if any kappa is not finite
+// Block-wide reduction: every thread passes its value; every thread gets the total.
+// Sums (Max = false) are added in a fixed order: wavefronts by xor butterfly, then the
+// waves in order.
+template <bool Max>
+__device__ __forceinline__ double block_total(double v) {
+  __shared__ double s_w[kWavesPerBlock];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const double o = __shfl_xor(v, off);
+    v = Max ? fmax(v, o) : v + o;
+  }
+  __syncthreads();  // s_w may still be read by a previous call
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double t = s_w[0];
+#pragma unroll
+  for (int w = 1; w < kWavesPerBlock; ++w) t = Max ? fmax(t, s_w[w]) : t + s_w[w];
+  return t;
+}
+
+// Total of value k of nparts partials of `stride` doubles each, in every thread.
+template <bool Max>
+__device__ __forceinline__ double reduce_block_parts(const double* __restrict__ part, int nparts,
+                                                     int stride, int k) {
+  double v = Max ? -INFINITY : 0.0;
+  for (int b = threadIdx.x; b < nparts; b += kBlock) {
+    const double x = part[static_cast<int64_t>(b) * stride + k];
+    v = Max ? fmax(v, x) : v + x;
+  }
+  return block_total<Max>(v);
+}
+
+// Block partials (-kappa_min, kappa_max, 1 if a kappa is not finite) -> part[3 b + 0..2]
 __global__ __launch_bounds__(kBlock) void k_minmax(const double* __restrict__ kappa, int64_t m,
-                                                   Tree tree, double* totals) {
-  __shared__ double s_w[kWavesPerBlock][3];
-  __shared__ double s_in[3], s_out[3];
+                                                   double* __restrict__ part) {
   double nmn = -INFINITY, mx = -INFINITY, bad = 0.0;
   for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < m;
        e += static_cast<int64_t>(gridDim.x) * kBlock) {
@@ -1286,40 +1321,33 @@ __global__ __launch_bounds__(kBlock) void k_minmax(const double* __restrict__ ka
       bad = 1.0;
     }
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    nmn = fmax(nmn, __shfl_xor(nmn, off));
-    mx = fmax(mx, __shfl_xor(mx, off));
-    bad = fmax(bad, __shfl_xor(bad, off));
-  }
-  if ((threadIdx.x & 63) == 0) {
-    s_w[threadIdx.x >> 6][0] = nmn;
-    s_w[threadIdx.x >> 6][1] = mx;
-    s_w[threadIdx.x >> 6][2] = bad;
-  }
-  __syncthreads();
-  if (threadIdx.x < 3) {
-    double s = s_w[0][threadIdx.x];
-    for (int w = 1; w < kWavesPerBlock; ++w) s = fmax(s, s_w[w][threadIdx.x]);
-    s_in[threadIdx.x] = s;
-  }
-  __syncthreads();
-  if (!tree_reduce<OpMax>(tree, 3, s_in, s_out)) return;
+  nmn = block_total<true>(nmn);
+  mx = block_total<true>(mx);
+  bad = block_total<true>(bad);
   if (threadIdx.x == 0) {
-    totals[0] = s_out[0];
-    totals[1] = s_out[1];
-    totals[4] = s_out[2];
+    double* o = part + 3 * static_cast<int64_t>(blockIdx.x);
+    o[0] = nmn;
+    o[1] = mx;
+    o[2] = bad;
   }
 }
 
-// q_u = sum_v (kappa_uv - kappa_min) / (kappa_max - kappa_min + eta) -> pn[u]; sum -> totals[2]
+// q_u = sum_v (kappa_uv - kappa_min) / (kappa_max - kappa_min + eta) -> pn[u]; block
+// partial sums -> part_n[b].  Block 0 also publishes totals[0] = -kappa_min,
+// totals[1] = kappa_max and totals[4] = the non-finite flag for the launches after it.
 __global__ __launch_bounds__(kBlock) void k_node_w(DevGraph g, const double* __restrict__ kappa,
-                                                   double eta, Tree tree, double* totals,
+                                                   double eta, const double* __restrict__ part_mm,
+                                                   int nmm, double* totals,
+                                                   double* __restrict__ part_n,
                                                    double* __restrict__ pn) {
-  __shared__ double s_w[kWavesPerBlock];
-  __shared__ double s_in[1], s_out[1];
-  const double kmin = -totals[0];
-  const double kmax = totals[1];
+  const double kmin = -reduce_block_parts<true>(part_mm, nmm, 3, 0);
+  const double kmax = reduce_block_parts<true>(part_mm, nmm, 3, 1);
+  const double bad = reduce_block_parts<true>(part_mm, nmm, 3, 2);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    totals[0] = -kmin;
+    totals[1] = kmax;
+    totals[4] = bad;
+  }
   const double den = kmax - kmin + eta;
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
@@ -1334,24 +1362,16 @@ __global__ __launch_bounds__(kBlock) void k_node_w(DevGraph g, const double* __r
     if (lane == 0) pn[i] = s;
     acc += s;  // identical in every lane
   }
-  if (lane == 0) s_w[wv] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double s = s_w[0];
-    for (int w = 1; w < kWavesPerBlock; ++w) s += s_w[w];
-    s_in[0] = s;
-  }
-  __syncthreads();
-  if (!tree_reduce<OpSum>(tree, 1, s_in, s_out)) return;
-  if (threadIdx.x == 0) totals[2] = s_out[0];
+  // one lane per wave carries the wave's sum into the block total
+  acc = block_total<false>(lane == 0 ? acc : 0.0);
+  if (threadIdx.x == 0) part_n[blockIdx.x] = acc;
 }
 
-// q_e = sqrt(max(2 kappa_max - kappa_e, 0)) + 1 -> pe[e]; sum -> totals[3]
+// q_e = sqrt(max(2 kappa_max - kappa_e, 0)) + 1 -> pe[e]; block partial sums -> part_e[b]
 __global__ __launch_bounds__(kBlock) void k_edge_w(const double* __restrict__ kappa, int64_t m,
-                                                   Tree tree, double* totals,
+                                                   const double* totals,
+                                                   double* __restrict__ part_e,
                                                    double* __restrict__ pe) {
-  __shared__ double s_w[kWavesPerBlock];
-  __shared__ double s_in[1], s_out[1];
   const double kmax = totals[1];
   double acc = 0.0;
   for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < m;
@@ -1360,26 +1380,24 @@ __global__ __launch_bounds__(kBlock) void k_edge_w(const double* __restrict__ ka
     pe[e] = q;
     acc += q;
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double s = s_w[0];
-    for (int w = 1; w < kWavesPerBlock; ++w) s += s_w[w];
-    s_in[0] = s;
-  }
-  __syncthreads();
-  if (!tree_reduce<OpSum>(tree, 1, s_in, s_out)) return;
-  if (threadIdx.x == 0) totals[3] = s_out[0];
+  acc = block_total<false>(acc);
+  if (threadIdx.x == 0) part_e[blockIdx.x] = acc;
 }
 
-__global__ __launch_bounds__(kBlock) void k_normalise(DevGraph g, const double* totals,
+// P_u = q_u / sum q, P_e = q_e / sum q_e (the sums reduced from the block partials of the
+// two previous launches); block 0 publishes them as totals[2] and totals[3].
+__global__ __launch_bounds__(kBlock) void k_normalise(DevGraph g, double* totals,
+                                                      const double* __restrict__ part_n, int nn,
+                                                      const double* __restrict__ part_e, int ne,
                                                       double inv_nonisolated,
                                                       double* __restrict__ pn,
                                                       double* __restrict__ pe) {
-  const double tn = totals[2];
-  const double te = totals[3];
+  const double tn = reduce_block_parts<false>(part_n, nn, 1, 0);
+  const double te = reduce_block_parts<false>(part_e, ne, 1, 0);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    totals[2] = tn;
+    totals[3] = te;
+  }
   // a NaN or infinite kappa (flagged by k_minmax) makes every probability NaN, rather
   // than letting the NaN weight fall back to the uniform distribution
   const bool bad = totals[4] != 0.0;
@@ -1727,19 +1745,20 @@ hipError_t launch_eids(const DevGraph& g, int32_t* out, hipStream_t s) {
 
 hipError_t launch_sampling(const DevGraph& g, const double* kappa, double eta, int64_t nonisolated,
                            const SampleWork& sw, double* pn, double* pe, hipStream_t s) {
+  // k_minmax and k_edge_w on sw.grid blocks, k_node_w on up to sw.grid blocks of 32 rows;
+  // the edge partials reuse the min/max partials' space (k_node_w has read them by then)
   const int grid = sw.grid;
-  ERC_LAUNCH(k_minmax, grid, s, kappa, g.m, sw.tree, sw.totals);
+  ERC_LAUNCH(k_minmax, grid, s, kappa, g.m, sw.part_mm);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const int gn = grid_for(g.n, kWavesPerBlock * 8, sw.grid);
-  // the node-weight tree needs its own grid size; reuse the same scratch (stream order)
-  ERC_LAUNCH(k_node_w, gn, s, g, kappa, eta, sw.tree, sw.totals, pn);
+  ERC_LAUNCH(k_node_w, gn, s, g, kappa, eta, sw.part_mm, grid, sw.totals, sw.part_n, pn);
   if ((err = hipGetLastError()) != hipSuccess) return err;
-  ERC_LAUNCH(k_edge_w, grid, s, kappa, g.m, sw.tree, sw.totals, pe);
+  ERC_LAUNCH(k_edge_w, grid, s, kappa, g.m, sw.totals, sw.part_mm, pe);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   const double inv = nonisolated > 0 ? 1.0 / static_cast<double>(nonisolated) : 0.0;
   const int gz = grid_for(g.n > g.m ? g.n : g.m, kBlock * 4, 4096);
-  ERC_LAUNCH(k_normalise, gz, s, g, sw.totals, inv, pn, pe);
+  ERC_LAUNCH(k_normalise, gz, s, g, sw.totals, sw.part_n, gn, sw.part_mm, grid, inv, pn, pe);
   return hipGetLastError();
 }
 

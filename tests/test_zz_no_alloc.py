@@ -63,7 +63,7 @@ def test_static_scratch_non_finite_curvature_gives_nan():
                                    pe.data_ptr(), torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     assert torch.isnan(pn).all() and torch.isnan(pe).all()
-    # and a finite call afterwards is clean again (the flag starts at zero every call)
+    # and a finite call afterwards is clean again (every call rewrites the flag)
     kappa[7] = 0.0
     _abi.erc_sampling_probs_static(G.handle, kappa.data_ptr(), 1e-12, pn.data_ptr(),
                                    pe.data_ptr(), torch.cuda.current_stream().cuda_stream)
