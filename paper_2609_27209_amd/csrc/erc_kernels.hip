@@ -1071,6 +1071,76 @@ __global__ __launch_bounds__(kBlock) void k_rhs(RhsArgs a) {
   for (int c = threadIdx.x; c < NP * KB; c += kBlock) part[c] = s_part[0][c];
 }
 
+// Unit weights, blocks of at most 64 columns: every term of a row's sum is +-1, so the
+// sum is an exact integer whatever the order of its terms, and the wavefront forms it
+// from ballots instead of a per-entry loop.  Lane l takes entry l of each 64-entry chunk
+// (orientation o_l = +1 when i < j, else -1; sign bits b_lc of the block's columns);
+// column c gains sum_l o_l (1 - 2 b_lc) = (|P| - |N|) - 2 (|P & B_c| - |N & B_c|) with
+// P, N the lanes of positive and negative orientation and B_c the lanes whose bit c is
+// set.  The integer times 1/sqrt(K), rounded once, is the same Y as the fp64 sum of
+// k_rhs; z, r, p and the y.y partials are written as there.
+template <typename T, int KB>
+__global__ __launch_bounds__(kBlock) void k_rhs_unit(RhsArgs a) {
+  static_assert(KB <= 64, "a block's columns span at most two sign words");
+  __shared__ DDv s_part[kWavesPerBlock][KB];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6;
+  T* __restrict__ Z = static_cast<T*>(a.z);
+  T* __restrict__ R = static_cast<T*>(a.r);
+  T* __restrict__ Pp = static_cast<T*>(a.p);
+  const int sh = a.col0 & 63;  // bit of the block's first column in its sign word
+  const bool two = sh + KB > 64;
+  Dot<T> r0;
+  const int nw = gridDim.x * kWavesPerBlock;
+  for (int i = blockIdx.x * kWavesPerBlock + wv; i < a.g.n; i += nw) {
+    int acc = 0;  // lane c < KB: column col0 + c of row i
+    const int64_t b = a.g.rowptr[i];
+    const int64_t e = a.g.rowptr[i + 1];
+    for (int64_t base = b; base < e; base += 64) {
+      const int cnt = static_cast<int>(min(static_cast<int64_t>(64), e - base));
+      const bool live = lane < cnt;
+      int myj = i, mye = 0;
+      if (live) {
+        myj = a.g.col[base + lane];
+        mye = a.g.eid[base + lane];
+      }
+      const uint64_t ctr0 = static_cast<uint64_t>(mye) * a.words + static_cast<uint64_t>(a.col0 >> 6);
+      const uint64_t w0 = splitmix_at(a.base, ctr0);
+      const uint64_t w1 = two ? splitmix_at(a.base, ctr0 + 1) : 0ull;
+      // bit c: the sign bit of global column col0 + c of this entry's edge
+      const uint64_t bits = sh == 0 ? w0 : ((w0 >> sh) | (w1 << (64 - sh)));
+      const uint64_t pos = __ballot(live && i < myj);
+      const uint64_t neg = __ballot(live && i > myj);
+      const int base_c = __popcll(pos) - __popcll(neg);
+#pragma unroll
+      for (int c = 0; c < KB; ++c) {
+        const uint64_t m = __ballot(live && ((bits >> c) & 1ull));
+        const int v = base_c - 2 * (__popcll(pos & m) - __popcll(neg & m));
+        acc += (lane == c) ? v : 0;
+      }
+    }
+    if (lane < KB) {
+      const T y = (lane < a.ncols) ? static_cast<T>(static_cast<double>(acc) * a.inv_sqrt_k) : T(0);
+      const int64_t o = static_cast<int64_t>(i) * KB + lane;
+      R[o] = y;
+      Z[o] = T(0);
+      Pp[o] = y;
+      r0.add(y, y);
+    }
+  }
+  if (lane < KB) s_part[wv][lane] = r0.get();
+  __syncthreads();
+  for (int c = threadIdx.x; c < KB; c += kBlock) {
+    DDv acc = s_part[0][c];
+#pragma unroll
+    for (int w = 1; w < kWavesPerBlock; ++w) acc = dd_add(acc, s_part[w][c]);
+    s_part[0][c] = acc;
+  }
+  __syncthreads();
+  DDv* part = reinterpret_cast<DDv*>(a.part) + static_cast<int64_t>(blockIdx.x) * KB;
+  for (int c = threadIdx.x; c < KB; c += kBlock) part[c] = s_part[0][c];
+}
+
 // rho_0 = y.y per column; initial CG state of the block (rho = y.M^-1 y with the
 // Jacobi variant).
 template <int KB>
@@ -1496,10 +1566,17 @@ hipError_t launch_fin_iter(const DevGraph& g, const Work& w, int mode, hipStream
 
 template <typename T, int KB>
 static hipError_t rhs_t(const RhsArgs& a, int grid, hipStream_t s) {
-  if (a.minv != nullptr)
+  if (a.minv != nullptr) {
     ERC_LAUNCH((k_rhs<T, KB, true>), grid, s, a);
-  else
+  } else {
+    if constexpr (KB <= 64) {
+      if (!a.g.weighted) {
+        ERC_LAUNCH((k_rhs_unit<T, KB>), grid, s, a);
+        return hipGetLastError();
+      }
+    }
     ERC_LAUNCH((k_rhs<T, KB, false>), grid, s, a);
+  }
   return hipGetLastError();
 }
 

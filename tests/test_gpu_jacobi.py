@@ -91,7 +91,7 @@ def test_unknown_flag_rejected():
     g = gen.make_graph("er2k")
     G = E.Graph(g.rowptr, g.col, g.w, "f64")
     prm = G.params(32, 32, 1e-6, 1e-8, 100, 1)
-    prm.flags = 16  # no flag has this bit
+    prm.flags = 32  # no flag has this bit
     ws = G.workspace(32)
     R = torch.empty(g.m, dtype=torch.float64, device="cuda")
     with pytest.raises(_abi.ErcError) as ei:

@@ -79,6 +79,24 @@ def test_rhs_bit_exact(dtype, K, col0, ncols):
     assert np.array_equal(Y.view(np.uint8), Yo.view(np.uint8))
 
 
+@pytest.mark.parametrize("dtype,K,col0,ncols", [
+    ("f32", 64, 0, 64), ("f32", 96, 40, 40), ("f32", 300, 17, 47), ("f32", 200, 150, 50),
+    ("f32", 60, 10, 50), ("f64", 32, 0, 32), ("f64", 100, 60, 8), ("f64", 130, 100, 30),
+    ("f32", 512, 128, 128)])
+def test_rhs_bit_exact_unit_weights(dtype, K, col0, ncols):
+    # unit weights take the integer (ballot) form of the row sums for blocks of up to 64
+    # columns, including blocks whose columns straddle two sign words and padded blocks;
+    # hub rows span several 64-entry chunks
+    E = _gpu()
+    g = gen.chung_lu(3000, 2.1, 2.0, 20000, seed=11, weighted=False)
+    assert g.w is None and g.degrees().max() > 130
+    G = _graph(E, g, dtype)
+    Y = G.debug_rhs(K, col0, ncols, seed=31).cpu().numpy()
+    Yo = OE.rhs(g, K, col0, ncols, 31, dtype)
+    assert Y.dtype == Yo.dtype
+    assert np.array_equal(Y.view(np.uint8), Yo.view(np.uint8))
+
+
 def test_rhs_bit_exact_hub_rows():
     # rows longer than 64 neighbours exercise the 64-wide prefetch windows
     E = _gpu()
