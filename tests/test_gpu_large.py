@@ -15,6 +15,9 @@ edges each, which take the long-row work paths of the SpMM):
 * kappa: error over its condition scale 2 (s_u + s_v) / R + |kappa| <= 1e-4;
 * sampling probabilities: within the first-order bound that the 1e-4 curvature
   tolerance induces through Eqs. 7-8 and the normalisation (stored per entry).
+
+cl170k_relabel is the 170k-node workload with node ids randomly permuted (no hub-first
+order; columns 0-7), which the oracle solved on the same relabelled graph.
 """
 import json
 import math
@@ -46,7 +49,8 @@ def _load(name):
     return json.loads(str(f["meta"])), f
 
 
-@pytest.mark.parametrize("tag", ["cl170k", "cl230k", "cl2400k", "cl2400k_jacobi"])
+@pytest.mark.parametrize("tag", ["cl170k", "cl170k_relabel", "cl230k", "cl2400k",
+                                 "cl2400k_jacobi"])
 def test_stored_oracle_parity(tag, parity_log):
     E = _gpu()
     meta, gold = _load(tag)
