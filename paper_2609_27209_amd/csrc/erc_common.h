@@ -104,7 +104,7 @@ struct Work {
   void* r;
   void* p;
   void* q;
-  void* chunkbuf;    // nchunk_slots x kb partial sums of multi-chunk rows
+  void* chunkbuf;    // nchunk_slots x kb fp64 partial sums of multi-chunk rows
   double* mega_dots; // nmega x 3 x kb compensated (s, c) pairs
   ColState cs;
   double* part;      // block partials of the SpMM / RHS launch: grid x 3 x kb pairs

@@ -523,7 +523,7 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.r = take(vecb);
   L.p = take(vecb);
   L.q = take(vecb);
-  L.chunkbuf = take(static_cast<int64_t>(h->dg.nchunk_slots) * kb * s);
+  L.chunkbuf = take(static_cast<int64_t>(h->dg.nchunk_slots) * kb * 8);  // fp64 chunk sums
   L.mega_dots = take(static_cast<int64_t>(h->dg.nmega) * 3 * kb * 16);
   L.rho = take(kb * 8);
   L.rr = take(kb * 8);

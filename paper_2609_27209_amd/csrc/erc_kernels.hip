@@ -70,6 +70,20 @@ __device__ __forceinline__ void stv_nt(T* p, const V<T>& v) {
   __builtin_nontemporal_store(e, reinterpret_cast<E*>(p));
 }
 
+// fp64 accumulator of one lane's V<T>::N columns: the sums over long rows (wavefront
+// rows, block tasks, split rows) are formed in fp64 whatever the working precision.
+template <typename T>
+struct A64 {
+  double x[V<T>::N];
+};
+template <typename T>
+__device__ __forceinline__ A64<T> azero() {
+  A64<T> a;
+#pragma unroll
+  for (int k = 0; k < V<T>::N; ++k) a.x[k] = 0.0;
+  return a;
+}
+
 template <typename T>
 __device__ __forceinline__ V<T> vzero() {
   V<T> v;
@@ -276,7 +290,10 @@ __device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
 
 // ---------------------------------------------------------------------------------
 // Neighbour gather of one row range: acc += w_ij (p_i - p_j) over CSR entries
-// [beg, end) of row i.  Lane (grp, sub) handles neighbour slot grp of each step and
+// [beg, end) of row i, in the working precision (acc a V<T>) or with each term formed
+// and added in fp64 (acc an A64<T>: the block tasks, whose rows hold thousands to tens
+// of thousands of entries, where an fp32 sum loses the small differences between a hub
+// and its neighbours).  Lane (grp, sub) handles neighbour slot grp of each step and
 // columns [sub*VEC, sub*VEC + VEC).  Each lane issues kInflight row loads before it
 // consumes them, so a wavefront keeps kInflight * 1 KB of gathers in flight.  Slots past
 // the end read p_i with weight 0, which adds exactly zero.
@@ -291,11 +308,12 @@ constexpr int kInflight = ERC_SPMM_INFLIGHT;
 #endif
 constexpr int kWaveRowMin = ERC_WAVE_ROW_MIN;
 
-template <typename T, int LPN, bool W>
+template <typename T, int LPN, bool W, typename ACC>
 __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
                                            const T* __restrict__ wgt, const T* __restrict__ P,
                                            int i, int64_t beg, int64_t end, const V<T>& pi,
-                                           V<T>& acc, int lane) {
+                                           ACC& acc, int lane) {
+  constexpr bool D = sizeof(ACC) > sizeof(V<T>);  // fp64 sums of an fp32 row
   constexpr int VEC = V<T>::N;
   constexpr int KB = LPN * VEC;
   constexpr int NPW = 64 / LPN;
@@ -310,11 +328,13 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
       if (W) myw = wgt[base + lane];
     }
     const int steps = (cnt + NPW - 1) / NPW;
-    for (int st = 0; st < steps; st += kInflight) {
-      V<T> pj[kInflight];
-      T wj[kInflight];
+    // fewer rows in flight with fp64 sums, which hold twice the accumulator registers
+    constexpr int NI = D ? kInflight / 2 : kInflight;
+    for (int st = 0; st < steps; st += NI) {
+      V<T> pj[NI];
+      T wj[NI];
 #pragma unroll
-      for (int u = 0; u < kInflight; ++u) {
+      for (int u = 0; u < NI; ++u) {
         const int k = (st + u) * NPW + grp;
         int j = __shfl(myj, k & 63);
         wj[u] = W ? __shfl(myw, k & 63) : T(1);
@@ -325,8 +345,13 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
         pj[u] = ldv(P + static_cast<int64_t>(j) * KB + sub * VEC);
       }
 #pragma unroll
-      for (int u = 0; u < kInflight; ++u) {
-        if (W) {
+      for (int u = 0; u < NI; ++u) {
+        if constexpr (D) {
+          const double w64 = W ? static_cast<double>(wj[u]) : 1.0;
+#pragma unroll
+          for (int v = 0; v < VEC; ++v)
+            acc.x[v] += w64 * (static_cast<double>(pi.x[v]) - static_cast<double>(pj[u].x[v]));
+        } else if (W) {
 #pragma unroll
           for (int v = 0; v < VEC; ++v) acc.x[v] += wj[u] * (pi.x[v] - pj[u].x[v]);
         } else {
@@ -340,8 +365,8 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
 
 // Sum acc over the NPW neighbour groups of the wavefront (xor butterfly: every lane
 // ends with the same, order-fixed total).
-template <typename T, int LPN>
-__device__ __forceinline__ void reduce_groups(V<T>& acc) {
+template <typename T, int LPN, typename ACC>
+__device__ __forceinline__ void reduce_groups(ACC& acc) {
 #pragma unroll
   for (int off = LPN; off < 64; off <<= 1) {
 #pragma unroll
@@ -377,7 +402,11 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   constexpr int KB = LPN * VEC;
   if (*a.gate == 0) return;
   __shared__ DDv s_dots[kWavesPerBlock][3 * KB];
-  __shared__ V<T> s_acc[kWavesPerBlock][LPN];
+  // the block tasks' per-wave sums share the LDS of the dot partials, which are written
+  // only after the last task's closing barrier
+  static_assert(sizeof(A64<T>) * kWavesPerBlock * LPN <= sizeof(DDv) * kWavesPerBlock * 3 * KB,
+                "block-task sums must fit the dot partials' LDS");
+  A64<T> (*s_acc)[LPN] = reinterpret_cast<A64<T> (*)[LPN]>(&s_dots[0][0]);
 
   const int lane = threadIdx.x & 63;
   const int wv = threadIdx.x >> 6;
@@ -394,13 +423,18 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
   // finished by group 0 of wave 0)
   Dot<T> ldots[3 * VEC];
 
-  // finish one row in group-0 lanes: q = delta p_i + acc, store, and accumulate the dots
-  // into this lane's partials
-  auto finish = [&](int i, const V<T>& pi, const V<T>& acc) {
+  // finish one row in group-0 lanes: q = delta p_i + acc (a block task's fp64 sum is
+  // rounded once), store, and accumulate the dots into this lane's partials
+  auto finish = [&](int i, const V<T>& pi, const auto& acc) {
     V<T> qv;
     const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + acc.x[v];
+    for (int v = 0; v < VEC; ++v) {
+      if constexpr (sizeof(acc) > sizeof(V<T>))
+        qv.x[v] = static_cast<T>(a.delta * static_cast<double>(pi.x[v]) + acc.x[v]);
+      else
+        qv.x[v] = dlt * pi.x[v] + acc.x[v];
+    }
     stv_nt(Q + off, qv);
     const V<T> ri = ldv_nt(Rr + off);
     const T mi = pc ? minv[i] : T(1);
@@ -421,16 +455,16 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
     const int64_t wb = tb + (len * wv) / kWavesPerBlock;
     const int64_t we = tb + (len * (wv + 1)) / kWavesPerBlock;
     const V<T> pi = ldv(P + static_cast<int64_t>(i) * KB + sub * VEC);
-    V<T> acc = vzero<T>();
+    A64<T> acc = azero<T>();
     gather_row<T, LPN, W>(a.g.col, wgt, P, i, wb, we, pi, acc, lane);
     reduce_groups<T, LPN>(acc);
     if (lane < LPN) s_acc[wv][sub] = acc;
     __syncthreads();
-    V<T> tot = vzero<T>();
+    A64<T> tot = azero<T>();
     if (wv == 0 && lane < LPN) {
 #pragma unroll
       for (int w = 0; w < kWavesPerBlock; ++w) {
-        const V<T> x = s_acc[w][sub];
+        const A64<T> x = s_acc[w][sub];
 #pragma unroll
         for (int v = 0; v < VEC; ++v) tot.x[v] += x.x[v];
       }
@@ -439,9 +473,12 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
       if (mh < 0) {
         finish(i, pi, tot);
       } else {
-        // one chunk of a split row: its sum goes to the row's chunk slot, k_mega_fin adds
-        T* cb = static_cast<T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
-        stv(cb + static_cast<int64_t>(a.g.task_chunk[t]) * KB + sub * VEC, tot);
+        // one chunk of a split row: its fp64 sum goes to the row's chunk slot, k_mega_fin
+        // adds the chunks
+        double* cb = static_cast<double*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB) +
+                     static_cast<int64_t>(a.g.task_chunk[t]) * KB + sub * VEC;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) cb[v] = tot.x[v];
       }
     }
     __syncthreads();
@@ -576,7 +613,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_spmm(SpmmArgs a) {
 }
 
 // Rows split over several blocks of the SpMM: one wavefront per row adds the row's
-// chunk sums in chunk order (the order the chunks cover the row), forms q_i =
+// fp64 chunk sums in chunk order (the order the chunks cover the row), forms q_i =
 // delta p_i + sum, and stores the row's p.q, r.q, q.q terms as its own compensated pairs
 // (nmega x 3 x kb), which k_fin_col adds to the column totals.  Running in the launch
 // after the SpMM makes the chunk sums visible without a device-scope fence.
@@ -590,25 +627,25 @@ __global__ __launch_bounds__(64) void k_mega_fin(SpmmArgs a) {
   if (sub >= LPN) return;
   const int i = a.g.mega_row[mh];
   const int nch = a.g.mega_nchunk[mh];
-  const T* __restrict__ cb =
-      static_cast<const T*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
-  V<T> rs = vzero<T>();
+  const double* __restrict__ cb =
+      static_cast<const double*>(a.chunkbuf) + a.g.mega_chunk0[mh] * static_cast<int64_t>(KB);
+  A64<T> rs = azero<T>();
   for (int k = 0; k < nch; ++k) {
-    const V<T> x = ldv(cb + static_cast<int64_t>(k) * KB + sub * VEC);
+    const double* x = cb + static_cast<int64_t>(k) * KB + sub * VEC;
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) rs.x[v] += x.x[v];
+    for (int v = 0; v < VEC; ++v) rs.x[v] += x[v];
   }
   const T* __restrict__ P = static_cast<const T*>(a.p);
   const T* __restrict__ Rr = static_cast<const T*>(a.r);
   T* __restrict__ Q = static_cast<T*>(a.q);
   const T* __restrict__ minv = static_cast<const T*>(a.minv);
   const bool pc = minv != nullptr;
-  const T dlt = static_cast<T>(a.delta);
   const int64_t off = static_cast<int64_t>(i) * KB + sub * VEC;
   const V<T> pi = ldv(P + off);
   V<T> qv;
 #pragma unroll
-  for (int v = 0; v < VEC; ++v) qv.x[v] = dlt * pi.x[v] + rs.x[v];
+  for (int v = 0; v < VEC; ++v)
+    qv.x[v] = static_cast<T>(a.delta * static_cast<double>(pi.x[v]) + rs.x[v]);
   stv_nt(Q + off, qv);
   const V<T> ri = ldv_nt(Rr + off);
   const T mi = pc ? minv[i] : T(1);
