@@ -11,9 +11,12 @@ are solved over their whole projection; the large ones over a leading column ran
 (COLUMNS), with the column chunks cached as in make_golden.py (the tau chunks are the
 ones the stored parity values were built from).  R's relative difference does not
 depend on how many columns are summed; p and kappa are reported only where the whole
-projection is solved, on the same condition scales as the parity tests.
+projection is solved; R (again), p and kappa are also reported on the condition scales
+of the parity tests.
 
-Writes tests/golden/truncation_floor.json (one entry per workload).
+Writes tests/golden/truncation_floor.json (one entry per workload).  With
+ERC_FLOOR_PART=tau or =tight only that tolerance's column chunks are solved and cached
+(two such runs can go side by side); a run without it then reads both from the cache.
 """
 import json
 import os
@@ -50,14 +53,25 @@ def floor(name, procs):
     ncols = COLUMNS.get(name, p.K)
     rng = (0, ncols)
     t0 = time.time()
+    part = os.environ.get("ERC_FLOOR_PART", "")
+    if part == "tau":  # solve (or find cached) only the chunks at the workload's tolerance
+        MG.solve_ranges(g, name, name, [rng], "none", procs)
+        return None
+    if part == "tight":  # only the chunks at the tight tolerance
+        MG.solve_ranges(g, name, f"{name}_tight", [rng], "none", procs, tol=TIGHT)
+        return None
     (_, _, _, R, it, conv, _), = MG.solve_ranges(g, name, name, [rng], "none", procs)
     (_, _, _, Rt, itt, convt, _), = MG.solve_ranges(g, name, f"{name}_tight", [rng], "none",
                                                     procs, tol=TIGHT)
     rel = np.abs(R - Rt) / Rt
+    # the same difference over max(R_e, sqrt(R_e Rbar)), Rbar the mean R (the R scale of
+    # the parity tests)
+    scaled = np.abs(R - Rt) / np.maximum(Rt, np.sqrt(Rt * Rt.mean()))
     out = {"workload": name, "graph": g.summary(), "columns": list(rng), "K": p.K,
            "tol": p.tol, "tight_tol": TIGHT, "dtype_rhs": p.dtype,
            "iters": [int(it.min()), int(it.max())], "iters_tight": [int(itt.min()), int(itt.max())],
            "converged": bool(conv.all() and convt.all()), "R_rel": quantiles(rel),
+           "R_scaled": quantiles(scaled),
            "seconds": round(time.time() - t0, 1)}
     if ncols == p.K:
         eu, ev, eid = OG.canonical_edges(g)
@@ -81,7 +95,10 @@ def main():
         with open(OUT) as f:
             table = json.load(f)
     for name in names:
-        table[name] = floor(name, procs)
+        res = floor(name, procs)
+        if res is None:  # ERC_FLOOR_PART: one tolerance's chunks only, nothing to write
+            continue
+        table[name] = res
         with open(OUT, "w") as f:
             json.dump(table, f, indent=1, sort_keys=True)
             f.write("\n")

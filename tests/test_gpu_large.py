@@ -10,7 +10,14 @@ shift, tolerance and seed; the 2.4M-node workload's stored ranges are its first
 ones, the two extreme-curvature edges, and the 256 highest-degree rows with up to 128
 edges each, which take the long-row work paths of the SpMM):
 
-* R: relative error <= 1e-4;
+* R: error over max(R_e, sqrt(R_e Rbar)) <= 1e-4, Rbar the mean of the stored R: plain
+  relative for edges at or above the mean, and, below it, relative to the geometric mean
+  of R_e and Rbar.  That is how an iterate error of uniform size over the nodes (what
+  the relative-residual stop bounds) enters the squared differences of Eq. 6.  Hub-hub
+  edges have R_e hundreds of times below the mean; there two fp64 CG runs that differ
+  only in how they round the inner products differ by 2.2e-4 in plain relative terms
+  and by 2.1e-5 on this scale (tests/golden/make_rounding_spread.py).  The plain
+  relative error is printed beside it;
 * p: error over s_u = 1/2 sum_v w_uv R_uv <= 1e-4;
 * kappa: error over its condition scale 2 (s_u + s_v) / R + |kappa| <= 1e-4;
 * sampling probabilities: within the first-order bound that the 1e-4 curvature
@@ -50,7 +57,7 @@ def _load(name):
 
 
 @pytest.mark.parametrize("tag", ["cl170k", "cl170k_relabel", "cl230k", "cl2400k",
-                                 "cl2400k_jacobi"])
+                                 "cl2400k_c240", "cl2400k_jacobi"])
 def test_stored_oracle_parity(tag, parity_log):
     E = _gpu()
     meta, gold = _load(tag)
@@ -82,7 +89,9 @@ def test_stored_oracle_parity(tag, parity_log):
     rtol = meta["rtol"]
     parity_log(tag, R=(R, gold["R"]), p=(pp, gold["p"]), kappa=(kk, gold["kappa"]),
                node_prob=(pn, gold["node_prob"]), edge_prob=(pe, gold["edge_prob"]))
-    rel_R = np.max(np.abs(R - gold["R"]) / gold["R"])
+    rel_R_plain = np.max(np.abs(R - gold["R"]) / gold["R"])
+    Rbar = float(np.mean(gold["R"]))
+    rel_R = np.max(np.abs(R - gold["R"]) / np.maximum(gold["R"], np.sqrt(gold["R"] * Rbar)))
     s = gold["s_node"]
     iso = s == 0
     assert np.all(pp[iso] == gold["p"][iso])
@@ -90,7 +99,8 @@ def test_stored_oracle_parity(tag, parity_log):
     err_k = np.max(np.abs(kk - gold["kappa"]) / gold["kappa_scale"])
     over_n = np.max(np.abs(pn - gold["node_prob"]) / gold["node_prob_bound"])
     over_e = np.max(np.abs(pe - gold["edge_prob"]) / gold["edge_prob_bound"])
-    print(f"{tag}: R {rel_R:.3e} p {err_p:.3e} kappa {err_k:.3e} node prob {over_n:.3f} "
+    print(f"{tag}: R {rel_R:.3e} (plain relative {rel_R_plain:.3e}) p {err_p:.3e} "
+          f"kappa {err_k:.3e} node prob {over_n:.3f} "
           f"edge prob {over_e:.3f} of bound; iters {info['iters_max']} "
           f"(oracle {meta['iters_max']})")
     assert rel_R <= rtol
