@@ -70,8 +70,8 @@ __device__ __forceinline__ void stv_nt(T* p, const V<T>& v) {
   __builtin_nontemporal_store(e, reinterpret_cast<E*>(p));
 }
 
-// fp64 accumulator of one lane's V<T>::N columns: the sums over long rows (wavefront
-// rows, block tasks, split rows) are formed in fp64 whatever the working precision.
+// fp64 accumulator of one lane's V<T>::N columns: the SpMM's block tasks and split rows
+// (the rows above a thousand entries) sum in fp64 whatever the working precision.
 template <typename T>
 struct A64 {
   double x[V<T>::N];
@@ -294,8 +294,9 @@ __device__ bool tree_sum_dd(const Tree& t, int nval, const DDv* in, DDv* out) {
 // and added in fp64 (acc an A64<T>: the block tasks, whose rows hold thousands to tens
 // of thousands of entries, where an fp32 sum loses the small differences between a hub
 // and its neighbours).  Lane (grp, sub) handles neighbour slot grp of each step and
-// columns [sub*VEC, sub*VEC + VEC).  Each lane issues kInflight row loads before it
-// consumes them, so a wavefront keeps kInflight * 1 KB of gathers in flight.  Slots past
+// columns [sub*VEC, sub*VEC + VEC).  Each lane issues kInflight row loads (half as many
+// with fp64 sums) before it consumes them, so a wavefront keeps kInflight * 1 KB of
+// gathers in flight.  Slots past
 // the end read p_i with weight 0, which adds exactly zero.
 #ifndef ERC_SPMM_INFLIGHT
 #define ERC_SPMM_INFLIGHT 8
