@@ -66,8 +66,11 @@ typedef struct erc_graph_s* erc_handle;
  *  w           host, nnz weights of type w_dtype, or NULL for unit weights; every
  *              weight finite and > 0, and w_ij == w_ji exactly
  *  w_dtype     type of w (ignored when w == NULL)
- *  solve_dtype working precision of the CG vectors: ERC_F32 (dot products and all
- *              accumulations are still fp64) or ERC_F64
+ *  solve_dtype working precision of the CG vectors: ERC_F32 or ERC_F64.  With
+ *              ERC_F32 the dot products, R, p, kappa and the probabilities are
+ *              still fp64, and the SpMM sums the rows it runs as block tasks
+ *              (more than max(1024, two wavefront shares) entries) in fp64 and the
+ *              other rows in fp32
  * The structure must be symmetric with no self-loops and no repeated entries; each
  * undirected edge is stored twice.  Isolated nodes are allowed. */
 typedef struct {
