@@ -49,18 +49,20 @@ from oracle.parallel import solve_chunks  # noqa: E402
 
 # column ranges for workloads whose full sketch is too long for the CPU oracle: on the
 # 2.4M-node graph one column-iteration of the fp64 oracle takes seconds and a column
-# needs ~480 iterations, so the stored ranges are the first 64-column block and the
-# last 16 columns (sign word 3 of the hash, the fourth block), both in the launch
-# configuration of the benchmark (64-column blocks)
-RANGES = {"cl2400k": [(0, 64), (240, 256)]}
+# needs ~480 iterations, so the stored ranges are the first 64-column block, the last
+# 16 columns (sign word 3 of the hash, the fourth block) and 16 columns at the start of
+# each middle block (sign words 1 and 2), all in the launch configuration of the
+# benchmark (64-column blocks)
+RANGES = {"cl2400k": [(0, 64), (240, 256), (64, 80), (128, 144)]}
 # the Jacobi-preconditioned variant keeps its stored range
 RANGES_JACOBI = {"cl2400k": [(0, 16)]}
 # ":relabel" runs the workload on a copy with node ids permuted by RELABEL_SEED (no
 # hub-first order), over these column ranges
-RANGES_RELABEL = {"cl170k": [(0, 8)]}
+RANGES_RELABEL = {"cl170k": [(0, 8)], "cl2400k": [(0, 8)]}
 RELABEL_SEED = 7
-# columns per oracle process (ERC_ORACLE_CHUNK overrides: 11 puts the 2.4M-node graph's
-# 80 stored columns on eight processes at once)
+# columns per oracle process (ERC_ORACLE_CHUNK overrides it: 11 put the 2.4M-node
+# graph's first 80 stored columns on eight processes at once; its other two ranges were
+# solved later in 8-column chunks on four)
 CHUNK = int(os.environ.get("ERC_ORACLE_CHUNK", "8"))
 SAMPLES = 8192
 NHUB = 256

@@ -4,9 +4,9 @@ tests/golden/<name>.npz is written by tests/golden/make_golden.py, which runs on
 CPU oracle on the same seeded graph and projection (<name>_jacobi.npz: the oracle's
 Jacobi-preconditioned CG, compared with the GPU's ERC_JACOBI variant).  The GPU runs
 the same column range in the launch configuration of bench.py (same K, block width,
-shift, tolerance and seed; the 2.4M-node workload's stored ranges are its first
-64-column block and columns 240-255 of its last block, the Jacobi variant's its first
-16 columns) and is compared at the stored samples of edges and nodes (seeded random
+shift, tolerance and seed; the 2.4M-node workload's stored ranges are its whole first
+64-column block, the first 16 columns of its second and third blocks (64-79, 128-143)
+and the last 16 of its fourth (240-255); the Jacobi variant's are its first 16 columns) and is compared at the stored samples of edges and nodes (seeded random
 ones, the two extreme-curvature edges, and the 256 highest-degree rows with up to 128
 edges each, which take the long-row work paths of the SpMM):
 
@@ -57,7 +57,8 @@ def _load(name):
 
 
 @pytest.mark.parametrize("tag", ["cl170k", "cl170k_relabel", "cl230k", "cl2400k",
-                                 "cl2400k_c240", "cl2400k_jacobi"])
+                                 "cl2400k_c64", "cl2400k_c128", "cl2400k_c240",
+                                 "cl2400k_jacobi"])
 def test_stored_oracle_parity(tag, parity_log):
     E = _gpu()
     meta, gold = _load(tag)
