@@ -330,7 +330,9 @@ __device__ __forceinline__ void gather_row(const int32_t* __restrict__ col,
     }
     const int steps = (cnt + NPW - 1) / NPW;
     // fewer rows in flight with fp64 sums, which hold twice the accumulator registers
-    constexpr int NI = D ? kInflight / 2 : kInflight;
+    // (a quarter for weighted rows at 8 lanes per row, the instantiation closest to the
+    // register cap: it spilled 35 registers at half, 19 at a quarter)
+    constexpr int NI = D ? ((W && LPN == 8) ? kInflight / 4 : kInflight / 2) : kInflight;
     for (int st = 0; st < steps; st += NI) {
       V<T> pj[NI];
       T wj[NI];
