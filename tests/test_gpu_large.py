@@ -143,3 +143,30 @@ def test_largest_full_sketch_properties():
     assert abs(wR / ref - 1.0) <= 6 * sd
     # Foster: sum_e w_e R_e = n - c for exact R; regularisation only lowers the mean
     assert wR / n_c <= 1.0 + 6 * math.sqrt(2.0 / (p.K * n_c))
+
+
+@pytest.mark.parametrize("name", ["cl2400k", "cl230k"])
+def test_block_width_changes_only_rounding(name):
+    """All K columns at the workload's block width and at half of it.  Each column runs
+    the same CG either way; only the SpMM's grouping of each row's fp32 sum (lanes per
+    row, rows per wavefront) differs, so the two R agree on every edge to rounding: on
+    the scale M_e = max(R_e, sqrt(R_e Rbar)) of the stored-value tests, within 1e-4.
+    The plain relative difference is printed beside it; it is largest where R_e is far
+    below the mean (edges between two hubs)."""
+    E = _gpu()
+    p = gen.CONFIGS[name].params
+    g = gen.make_graph(name)
+    G = E.Graph(g.rowptr, g.col, g.w, solve_dtype=p.dtype)
+    Ra, ia = G.resistance(p.K, p.k_block, p.delta, p.tol, p.max_iter, p.seed)
+    Ra = Ra.clone()
+    Rb, ib = G.resistance(p.K, p.k_block // 2, p.delta, p.tol, p.max_iter, p.seed)
+    for info in (ia, ib):
+        assert info["cols_unconverged"] == 0 and info["breakdowns"] == 0
+    diff = (Ra - Rb).abs()
+    M = torch.maximum(Ra, torch.sqrt(Ra * Ra.mean()))
+    scaled = float((diff / M).max().item())
+    plain = float((diff / Ra).max().item())
+    print(f"{name}: block width {p.k_block} against {p.k_block // 2}: R {scaled:.3e} "
+          f"(plain relative {plain:.3e}) over all {g.m} edges; iterations "
+          f"{ia['iters_max']} / {ib['iters_max']}")
+    assert scaled <= 1e-4
