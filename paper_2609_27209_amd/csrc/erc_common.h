@@ -83,9 +83,8 @@ struct ColState {
   int32_t* pred_done;  // one int: every active column is predicted to stop after the
                        // pending update, so its exact test runs before the next SpMM
   int32_t* nspmm;      // one int: SpMM launches of this block that found active columns
-  uint32_t* fin_cnt;   // finishing-step counters: active columns, predicted-live flag and
-  uint32_t* fin_live;  // the blocks done; zero between launches
-  uint32_t* fin_tick;
+  unsigned long long* fin_word;  // finishing-step counter word: active columns, columns
+                                 // predicted to go on and blocks done; zero between launches
   int32_t* one;       // one int holding 1 (keeps debug launches from exiting early)
 };
 

@@ -546,7 +546,7 @@ WorkLayout work_layout(const erc_graph_s* h, int kb) {
   L.upd_pending = take(4);
   L.pred_done = take(4);
   L.nspmm = take(4);
-  L.fin_ctr = take(3 * 4);
+  L.fin_ctr = take(8);
   L.one = take(4);
   const int64_t nval = 10 * kb;  // up to five compensated (s, c) pairs per column
   L.part = take(static_cast<int64_t>(L.grid_tree) * 6 * kb * 8);
@@ -585,9 +585,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
   w.cs.upd_pending = reinterpret_cast<int32_t*>(b + L.upd_pending);
   w.cs.pred_done = reinterpret_cast<int32_t*>(b + L.pred_done);
   w.cs.nspmm = reinterpret_cast<int32_t*>(b + L.nspmm);
-  w.cs.fin_cnt = reinterpret_cast<uint32_t*>(b + L.fin_ctr);
-  w.cs.fin_live = w.cs.fin_cnt + 1;
-  w.cs.fin_tick = w.cs.fin_cnt + 2;
+  w.cs.fin_word = reinterpret_cast<unsigned long long*>(b + L.fin_ctr);
   w.cs.one = reinterpret_cast<int32_t*>(b + L.one);
   w.part = reinterpret_cast<double*>(b + L.part);
   w.part_u = reinterpret_cast<double*>(b + L.part_u);
@@ -613,7 +611,7 @@ Work carve_work(const erc_graph_s* h, int kb, void* ws, const WorkLayout& L, int
 // records no memset node).
 erc_status prepare_work(const erc_graph_s* h, const Work& w, const WorkLayout& L, hipStream_t s) {
   ERC_HIP(launch_fill_u32(w.tree.tick, 0u, tree_ticks(kMaxTreeGrid), s));
-  ERC_HIP(launch_fill_u32(w.cs.fin_cnt, 0u, 3, s));
+  ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.fin_word), 0u, 2, s));
   ERC_HIP(launch_fill_u32(reinterpret_cast<uint32_t*>(w.cs.one), 1u, 1, s));
   return ERC_OK;
 }

@@ -705,55 +705,71 @@ struct IterArgs {
 };
 
 // The per-iteration finishing step, in two launches without device-scope fences:
-//  k_fin_sum  (ceil(parts/32) blocks) level-1 sums of the block partials of the
-//             previous update (r.r, and r.M^-1 r with the Jacobi variant) and of this
-//             SpMM (p.q, r.q, q.q; M^-1-weighted r.q, q.q with the Jacobi variant),
+//  k_fin_sum  (ceil(parts/32) x ceil(values/64) blocks) level-1 sums of the block
+//             partials of the previous update (r.r, and r.M^-1 r with the Jacobi
+//             variant) and of this SpMM (p.q, r.q, q.q; M^-1-weighted r.q, q.q with
+//             the Jacobi variant),
 //             stored value-major so that the next launch reads them contiguously;
 //             skipped when the partial sets are short (k_fin_col then reads them);
 //  k_fin_col  (one block per column) the grid totals of its column in a fixed order,
 //             then (1) the stopping test of the pending update, r.r <= tol^2 rho_0,
 //             and rho = r.r (or r.M^-1 r), and (2) alpha = rho / p.q and, for the
 //             direction update, rho' = rho - 2 alpha r.q + alpha^2 q.q, i.e. the new rho
-//             expanded in double-double.  Integer atomics collect the active-column
-//             count; the last block to finish publishes it.
+//             expanded in double-double.  One integer atomic per block collects the
+//             active-column count; the last block to finish publishes it.
 // mode 0: both steps; 1: the stopping test only; 2: the stopping test only, and only
 // when the previous mode-0 step predicted that every active column stops.
 constexpr int kFinDirectMax = 2048;  // longest partial set k_fin_col sums by itself
+constexpr unsigned long long kFinField = (1ull << 20) - 1;  // one field of the counter word
+
+// k_fin_sum's grid is (groups of kTreeFan partials) x (64-value slices): each wavefront
+// of a block adds one quarter of its group's partials for 64 consecutive values, all of
+// its loads issued before they are added, and wavefront 0 then adds the quarters in
+// order, so every level-1 sum waits on one round of loads.
+constexpr int kFinWaves = kBlock / 64;
+constexpr int kFinPer = kTreeFan / kFinWaves;  // partials per wavefront and value
+static_assert(kTreeFan % kFinWaves == 0, "a partial group must split over the wavefronts");
 
 template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_sum(IterArgs a) {
   if (*a.cs.n_active == 0) return;
   if (a.mode == 2 && *a.cs.pred_done == 0) return;
+  __shared__ DDv s_q[kFinWaves][64];
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
   const int su = (a.pc ? 2 : 1) * KB;  // update values first, then the SpMM's three
   const int nval = su + 3 * KB;
-  DDv* l0 = reinterpret_cast<DDv*>(a.tree.lvl0);
-  const int b0 = blockIdx.x * kTreeFan;
-  for (int v = threadIdx.x; v < nval; v += kBlock) {
+  const int lane = threadIdx.x & 63;
+  const int wq = threadIdx.x >> 6;
+  const int v = blockIdx.y * 64 + lane;
+  DDv acc = DDv{0.0, 0.0};
+  if (v < nval) {
     const bool isu = v < su;
     const DDv* part = reinterpret_cast<const DDv*>(isu ? a.part_u : a.part_s);
     const int np = isu ? a.nparts_u : a.nparts_s;
     const int pv = isu ? su : 3 * KB;
     const int vv = isu ? v : v - su;
-    const int nb = min(kTreeFan, np - b0);
-    DDv acc = DDv{0.0, 0.0};
-    if ((isu ? upd : dots) && nb > 0) {
-      // partials in block order; eight loads are issued before they are added, so the
-      // sum is the same as one at a time
-      const DDv* src = part + static_cast<int64_t>(b0) * pv + vv;
-      acc = src[0];
-      int k = 1;
-      for (; k + 8 <= nb; k += 8) {
-        DDv x[8];
+    const int k0 = blockIdx.x * kTreeFan + wq * kFinPer;
+    const int cnt = min(kFinPer, np - k0);
+    if ((isu ? upd : dots) && cnt > 0) {
+      // this wavefront's partials in block order
+      const DDv* src = part + static_cast<int64_t>(k0) * pv + vv;
+      DDv x[kFinPer];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) x[u] = src[static_cast<int64_t>(k + u) * pv];
+      for (int u = 0; u < kFinPer; ++u)
+        x[u] = u < cnt ? src[static_cast<int64_t>(u) * pv] : DDv{0.0, 0.0};
+      acc = x[0];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) acc = dd_add(acc, x[u]);
-      }
-      for (; k < nb; ++k) acc = dd_add(acc, src[static_cast<int64_t>(k) * pv]);
+      for (int u = 1; u < kFinPer; ++u)
+        if (u < cnt) acc = dd_add(acc, x[u]);
     }
-    l0[static_cast<int64_t>(v) * gridDim.x + blockIdx.x] = acc;
+  }
+  s_q[wq][lane] = acc;
+  __syncthreads();
+  if (wq == 0 && v < nval) {
+#pragma unroll
+    for (int q = 1; q < kFinWaves; ++q) acc = dd_add(acc, s_q[q][lane]);
+    reinterpret_cast<DDv*>(a.tree.lvl0)[static_cast<int64_t>(v) * gridDim.x + blockIdx.x] = acc;
   }
 }
 
@@ -763,7 +779,7 @@ template <int KB>
 __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
   if (*a.cs.n_active == 0) return;
   if (a.mode == 2 && *a.cs.pred_done == 0) return;
-  __shared__ DDv s_red[5][kBlock];
+  __shared__ DDv s_red[5][kBlock / 64];
   __shared__ int s_last;
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
@@ -816,17 +832,25 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
           acc = dd_add(acc, md[static_cast<int64_t>(mh) * 3 * KB]);
       }
     }
-    s_red[k][tid] = acc;
+    // fold the wavefront's 64 sums (xor butterfly: every lane ends with the same,
+    // order-fixed total); the block's four wavefront totals are added below in order
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      DDv y;
+      y.s = __shfl_xor(acc.s, off);
+      y.c = __shfl_xor(acc.c, off);
+      acc = dd_add(acc, y);
+    }
+    if ((tid & 63) == 0) s_red[k][tid >> 6] = acc;
   }
   __syncthreads();
-  for (int w = kBlock / 2; w > 0; w >>= 1) {
-    if (tid < w) {
-#pragma unroll
-      for (int k = 0; k < 5; ++k) s_red[k][tid] = dd_add(s_red[k][tid], s_red[k][tid + w]);
-    }
-    __syncthreads();
-  }
   if (tid == 0) {
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+      DDv t = s_red[k][0];
+      for (int w = 1; w < kBlock / 64; ++w) t = dd_add(t, s_red[k][w]);
+      s_red[k][0] = t;
+    }
     int live = 0;
     if (upd && a.cs.active[c]) {
       const double rn = dd_value(s_red[0][0]);
@@ -870,14 +894,19 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
       a.cs.alpha[c] = 0.0;
       a.cs.beta[c] = 0.0;
     }
-    if (a.cs.active[c]) atomicAdd(a.cs.fin_cnt, 1u);
-    if (live) atomicOr(a.cs.fin_live, 1u);
-    s_last = atomicAdd(a.cs.fin_tick, 1u) == static_cast<unsigned>(gridDim.x - 1);
+    // one atomic per block on one word: active columns (bits 40-59), columns predicted
+    // to go on (bits 20-39) and blocks done (bits 0-19); the block that adds last reads
+    // the totals from the sum and clears the word for the next launch
+    const unsigned long long add = (static_cast<unsigned long long>(a.cs.active[c] ? 1 : 0) << 40) |
+                                   (static_cast<unsigned long long>(live) << 20) | 1ull;
+    const unsigned long long old = atomicAdd(a.cs.fin_word, add);
+    s_last = (old & kFinField) == static_cast<unsigned long long>(gridDim.x - 1);
     if (s_last) {
-      // every other block has added its column: publish the totals, reset the counters
-      const int cnt = static_cast<int>(atomicExch(a.cs.fin_cnt, 0u));
-      const bool any_live = atomicExch(a.cs.fin_live, 0u) != 0u;
-      atomicExch(a.cs.fin_tick, 0u);
+      // every other block has added its column: publish the totals, reset the word
+      const unsigned long long tot = old + add;
+      const int cnt = static_cast<int>((tot >> 40) & kFinField);
+      const bool any_live = ((tot >> 20) & kFinField) != 0;
+      atomicExch(a.cs.fin_word, 0ull);
       *a.cs.n_active = cnt;
       *a.cs.upd_pending = (dots && cnt > 0) ? 1 : 0;
       *a.cs.pred_done = (dots && cnt > 0 && !any_live) ? 1 : 0;
@@ -1564,7 +1593,10 @@ static hipError_t fin_iter_launch(const IterArgs& f, hipStream_t s) {
   const int np = f.nparts_s > f.nparts_u ? f.nparts_s : f.nparts_u;
   // short partial sets are summed by k_fin_col directly (one launch instead of two)
   const int nsum = np > kFinDirectMax ? (np + kTreeFan - 1) / kTreeFan : 0;
-  if (nsum > 0) ERC_LAUNCH((k_fin_sum<KB>), nsum, s, f);
+  if (nsum > 0) {
+    const int nval = (f.pc ? 2 : 1) * KB + 3 * KB;
+    ERC_LAUNCH((k_fin_sum<KB>), dim3(nsum, (nval + 63) / 64), s, f);
+  }
   ERC_LAUNCH((k_fin_col<KB>), KB, s, f, nsum);
   return hipGetLastError();
 }
