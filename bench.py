@@ -564,6 +564,59 @@ def gather_slices(name: str, torch, reps: int = 5):
             "indices": int(idx.numel()), "kernel": "k_probe_gather", "rows": rows}
 
 
+def _kernel_label(name: str) -> str:
+    """Short kernel name of a rocprofv3 record (the template arguments kept)."""
+    import re
+
+    m = re.search(r"(k_\w+<[^>]*>|k_\w+|__amd\w+|\w*elementwise\w*)", name)
+    return m.group(1) if m else name[:60]
+
+
+def trace_table(path: str, full_us: float = 20.0, min_ms: float = 0.0) -> str:
+    """Markdown table of a rocprofv3 kernel trace (its *_kernel_trace.csv): dispatches,
+    total and average duration per kernel, and the average over "full" dispatches (those
+    longer than full_us; launches after the last column converged return at once)."""
+    import collections
+    import csv
+
+    d = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            d[_kernel_label(r["Kernel_Name"])].append(
+                int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    tot = sum(sum(v) for v in d.values())
+    out = ["| kernel | dispatches | total ms | avg us (all) | avg us (> 20 us) | full | share |",
+           "|---|---|---|---|---|---|---|"]
+    for k, v in sorted(d.items(), key=lambda kv: -sum(kv[1])):
+        if sum(v) / 1e6 < min_ms:
+            continue
+        full = [x for x in v if x > full_us * 1e3]
+        avgf = sum(full) / len(full) / 1e3 if full else 0.0
+        out.append(f"| {k} | {len(v)} | {sum(v) / 1e6:.1f} | {sum(v) / len(v) / 1e3:.1f} | "
+                   f"{avgf:.1f} | {len(full)} | {100 * sum(v) / tot:.1f}% |")
+    return "\n".join(out)
+
+
+def counter_table(path: str, full_us: float = 20.0) -> str:
+    """Per kernel of a rocprofv3 counter run (its *_counter_collection.csv): dispatches,
+    full dispatches and the median counter value over the full ones."""
+    import collections
+    import csv
+    import statistics
+
+    d = collections.defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            d[(_kernel_label(r["Kernel_Name"]), r["Counter_Name"])].append(
+                (float(r["Counter_Value"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    out = ["| kernel | counter | dispatches | full | median (full) |", "|---|---|---|---|---|"]
+    for (k, c), v in d.items():
+        full = [x for x, dur in v if dur > full_us * 1e3]
+        med = f"{statistics.median(full):.1f}" if full else "-"
+        out.append(f"| {k} | {c} | {len(v)} | {len(full)} | {med} |")
+    return "\n".join(out)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -601,7 +654,22 @@ def main() -> int:
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the timed steps, copy a buffer of this size 3 times (a plain "
                          "copy kernel of known size, to calibrate HBM byte counters)")
+    ap.add_argument("--trace-table", default=None, metavar="CSV",
+                    help="print the per-kernel table of a rocprofv3 kernel trace "
+                         "(*_kernel_trace.csv) and exit (no GPU needed)")
+    ap.add_argument("--counter-table", action="append", default=None, metavar="CSV",
+                    help="print the per-kernel median counter values of a rocprofv3 --pmc "
+                         "run (*_counter_collection.csv; may be given more than once) and "
+                         "exit (no GPU needed)")
+    ap.add_argument("--table-min-ms", type=float, default=0.0,
+                    help="with --trace-table: list only kernels with at least this many ms")
     args = ap.parse_args()
+    if args.trace_table or args.counter_table:
+        if args.trace_table:
+            print(trace_table(args.trace_table, min_ms=args.table_min_ms))
+        for path in args.counter_table or []:
+            print(counter_table(path))
+        return 0
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the column "
               "sharding over several GPUs (a range of columns per GPU, then one sum of R) "

@@ -136,3 +136,27 @@ def test_block_sweep(monkeypatch, capsys):
     for k in (1, 2):
         assert mem[k] - mem[0] >= 4 * n * (rows[k]["k_block"] - rows[0]["k_block"]) * 4
     assert all(r["ms_per_step"] > 0 and r["iters_max"] > 0 for r in rows)
+
+
+def test_trace_and_counter_tables(tmp_path, monkeypatch, capsys):
+    # rocprofv3's CSV columns; two kernels, one with a short (early-exit) dispatch
+    tr = tmp_path / "t_kernel_trace.csv"
+    tr.write_text(
+        "Kernel_Name,Start_Timestamp,End_Timestamp\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",0,4000000\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",5000000,9000000\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",9000000,9002000\n"
+        "\"void erc::k_update<float, 16, false>(erc::UpdArgs)\",9100000,9900000\n")
+    ct = tmp_path / "c_counter_collection.csv"
+    ct.write_text(
+        "Kernel_Name,Counter_Name,Counter_Value,Start_Timestamp,End_Timestamp\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",FETCH_SIZE,10,0,4000000\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",FETCH_SIZE,30,0,4000000\n"
+        "\"void erc::k_spmm<float, 16, true>(erc::SpmmArgs)\",FETCH_SIZE,1,0,2000\n")
+    assert _main(monkeypatch, "--trace-table", str(tr), "--counter-table", str(ct)) == 0
+    out = capsys.readouterr().out
+    # 3 dispatches, 8.002 ms in all, 4 ms per full dispatch (2 of them)
+    assert "| k_spmm<float, 16, true> | 3 | 8.0 | 2667.3 | 4000.0 | 2 | 90.9% |" in out
+    assert "| k_update<float, 16, false> | 1 | 0.8 | 800.0 | 800.0 | 1 | 9.1% |" in out
+    # median over the two full dispatches only
+    assert "| k_spmm<float, 16, true> | FETCH_SIZE | 3 | 2 | 20.0 |" in out
