@@ -79,7 +79,6 @@ constexpr int kMaxGridUpd = 32768;
 static_assert((kMaxGridUpd + kTreeFan - 1) / kTreeFan <= kMaxTreeGrid,
               "level-1 sums of the update partials must fit the tree buffers");
 constexpr int kMaxGridEd = 8192;
-constexpr int kCountBadGrid = kMaxTreeGrid;
 // Grid cap of the sampling passes: their scratch is 4 doubles per block plus 64 bytes,
 // 33 KB at the cap, inside the fixed scratch of erc_sampling_probs_static.
 constexpr int kSampleGrid = 1024;

@@ -784,7 +784,6 @@ __global__ __launch_bounds__(kBlock) void k_fin_col(IterArgs a, int nsum) {
   const bool upd = *a.cs.upd_pending != 0;
   const bool dots = a.mode == 0;
   const int su = (a.pc ? 2 : 1) * KB;
-  const int nval = su + 3 * KB;
   const int c = blockIdx.x;
   const int tid = threadIdx.x;
   // value slots of this column: r.r, r.M^-1 r, p.q, r.q, q.q
