@@ -49,11 +49,11 @@ from oracle.parallel import solve_chunks  # noqa: E402
 
 # column ranges for workloads whose full sketch is too long for the CPU oracle: on the
 # 2.4M-node graph one column-iteration of the fp64 oracle takes seconds and a column
-# needs ~480 iterations, so the stored ranges are the first 64-column block, the last
-# 16 columns (sign word 3 of the hash, the fourth block) and 16 columns at the start of
-# each middle block (sign words 1 and 2), all in the launch configuration of the
+# needs ~480 iterations, so the stored ranges are the first two 64-column blocks (sign
+# words 0 and 1 of the hash), the last 16 columns (sign word 3, the fourth block) and
+# the first 16 of the third block (sign word 2), all in the launch configuration of the
 # benchmark (64-column blocks)
-RANGES = {"cl2400k": [(0, 64), (240, 256), (64, 80), (128, 144)]}
+RANGES = {"cl2400k": [(0, 64), (240, 256), (64, 128), (128, 144)]}
 # the Jacobi-preconditioned variant keeps its stored range
 RANGES_JACOBI = {"cl2400k": [(0, 16)]}
 # ":relabel" runs the workload on a copy with node ids permuted by RELABEL_SEED (no

@@ -5,7 +5,7 @@ CPU oracle on the same seeded graph and projection (<name>_jacobi.npz: the oracl
 Jacobi-preconditioned CG, compared with the GPU's ERC_JACOBI variant).  The GPU runs
 the same column range in the launch configuration of bench.py (same K, block width,
 shift, tolerance and seed; the 2.4M-node workload's stored ranges are its whole first
-64-column block, the first 16 columns of its second and third blocks (64-79, 128-143)
+and second 64-column blocks (0-63, 64-127), the first 16 columns of its third (128-143)
 and the last 16 of its fourth (240-255); the Jacobi variant's are its first 16 columns) and is compared at the stored samples of edges and nodes (seeded random
 ones, the two extreme-curvature edges, and the 256 highest-degree rows with up to 128
 edges each, which take the long-row work paths of the SpMM):
